@@ -1,0 +1,32 @@
+"""fp64 CPU oracle of the ESTP scoring and pooling path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it, to check and to time the HIP
+library against plain, slow definitions.  It shares no code with the HIP path.
+
+Every function takes bf16 bit patterns (uint16) or float arrays, widens them
+exactly to float64 and evaluates the paper's definitions:
+
+* ``token_entropy``      - Eq. 2 (Section 4.2)
+* ``attn_importance``    - Eq. 1 (Section 4.1)
+* ``combine_weights``    - Eq. 3 and Eq. 4 (Section 4.2)
+* ``pool``               - Eq. 5 (Section 4.2)
+* ``predict``            - the MLP length head with Eq. 7 (Section 4.3)
+* ``soft_labels``, ``length_loss`` - Eq. 6 and Eq. 8 (Section 4.3)
+
+``oracle.bruteforce`` re-derives the same quantities with pure-Python loops
+for tiny shapes; the tests pin this module against it, against closed forms
+and against invariants the definitions fix.
+"""
+from .estp_oracle import (  # noqa: F401
+    widen,
+    token_entropy,
+    attn_importance,
+    combine_weights,
+    pool,
+    predict,
+    soft_labels,
+    length_loss,
+    run_path,
+)

@@ -1,0 +1,244 @@
+"""Plain fp64 definitions of the ESTP scoring and pooling path.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): the product path never
+imports this module.
+
+Notation follows the paper: hidden states h_i (here rows of ``X``), entropy
+H_i (Eq. 2), attention importance S_j (Eq. 1), fused score T_i (Eq. 3),
+pooling weights e_i (Eq. 4), pooled representation h (Eq. 5), bin
+probabilities p-hat and expected length y-hat (Eq. 7).
+
+Readings of points the paper leaves open (each is also listed with its
+reason in the design notes of the repository):
+
+* H_i is the entropy of the LM-head distribution computed from token i's own
+  final-layer hidden state, for every prompt token including the last; the LM
+  head is ``W @ h_i`` with no bias, scaling or cap; natural log (nats).
+* A is the causal self-attention of one layer averaged over the Hq query
+  heads; the diagonal A_jj is part of the sum in Eq. 1; the normaliser is the
+  prompt's own length N; with several layers the per-layer S are summed.
+  Scores are ``scale * q_i . k_j`` with ``scale = 1/sqrt(dh)`` on post-RoPE
+  queries and keys; query head h reads key head ``h // (Hq // Hkv)``.
+* Eq. 4 is read with the temperature the text names: e = softmax(T / alpha).
+* ``norm="zscore"`` replaces S and H by their per-prompt z-scores before
+  Eq. 3 (population std, epsilon 1e-6); ``norm="none"`` is Eq. 3 literally.
+* ties (top token, bin argmax) go to the lowest index; the shortest-job-first
+  order is a stable ascending sort of y-hat.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+
+
+# ----------------------------------------------------------------------------- inputs
+
+def widen(a) -> np.ndarray:
+    """Exact float64 copy of bf16 bit patterns (uint16) or of a float array."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+# ----------------------------------------------------------------------------- Eq. 2
+
+def token_entropy(X, W, row_chunk: int = 64) -> np.ndarray:
+    """H_i = -sum_v P(v) log P(v), P = softmax over the vocabulary of W h_i (Eq. 2).
+
+    ``X`` [n, d] hidden states, ``W`` [V, d] LM-head weight.  Rows are
+    processed ``row_chunk`` at a time only to bound memory; every row sees its
+    complete logit vector.
+    """
+    Xd = widen(X)
+    Wd = widen(W)
+    n = Xd.shape[0]
+    H = np.empty(n, dtype=np.float64)
+    for r0 in range(0, n, row_chunk):
+        z = Xd[r0:r0 + row_chunk] @ Wd.T                      # logits, [rows, V]
+        m = z.max(axis=1, keepdims=True)
+        lse = m + np.log(np.exp(z - m).sum(axis=1, keepdims=True))   # log of the partition sum
+        logp = z - lse                                         # log P(v)
+        p = np.exp(logp)
+        H[r0:r0 + row_chunk] = -(p * logp).sum(axis=1)
+    return H
+
+
+# ----------------------------------------------------------------------------- Eq. 1
+
+def _causal_softmax_rows(s: np.ndarray, i0: int) -> np.ndarray:
+    """Row-wise softmax of scores s [rows, N] for queries i0.., keys j <= i only."""
+    rows, N = s.shape
+    i = np.arange(i0, i0 + rows)[:, None]
+    j = np.arange(N)[None, :]
+    s = np.where(j <= i, s, -np.inf)
+    m = s.max(axis=1, keepdims=True)
+    p = np.exp(s - m)
+    return p / p.sum(axis=1, keepdims=True)
+
+
+def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: int = 2048) -> np.ndarray:
+    """S_j = (1/N) sum_i A_ij with A the head-averaged causal attention (Eq. 1).
+
+    ``Q`` [L, n_tok, Hq, dh] and ``K`` [L, n_tok, Hkv, dh] are post-RoPE
+    queries and keys of L layers, packed over prompts by ``cu_seqlens``
+    [B+1]; the result [n_tok] sums the per-layer importance.  Query rows are
+    taken ``row_chunk`` at a time (the column sum over i is split into
+    consecutive ranges); each attention row is complete.
+    """
+    Qd = widen(Q)
+    Kd = widen(K)
+    if Qd.ndim == 3:
+        Qd, Kd = Qd[None], Kd[None]
+    L, n_tok, Hq, dh = Qd.shape
+    Hkv = Kd.shape[2]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    S = np.zeros(n_tok, dtype=np.float64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        N = hi - lo
+        if N <= 0:
+            continue
+        for l in range(L):
+            colsum = np.zeros(N, dtype=np.float64)           # sum_i of the head-averaged A_ij
+            for h in range(Hq):
+                q = Qd[l, lo:hi, h, :]
+                k = Kd[l, lo:hi, h // G, :]
+                for i0 in range(0, N, row_chunk):
+                    s = scale * (q[i0:i0 + row_chunk] @ k.T)
+                    A = _causal_softmax_rows(s, i0)
+                    colsum += A.sum(axis=0) / Hq
+            S[lo:hi] += colsum / N
+    return S
+
+
+# ----------------------------------------------------------------------------- Eq. 3, 4
+
+def _zscore(v: np.ndarray, eps: float = 1e-6) -> np.ndarray:
+    return (v - v.mean()) / (v.std() + eps)
+
+
+def combine_weights(S, H, cu_seqlens, lambda1: float, lambda2: float, alpha: float = 1.0,
+                    norm: str = "none"):
+    """T_i = lambda1 S_i + lambda2 H_i (Eq. 3); e = softmax over the prompt of T / alpha (Eq. 4).
+
+    Returns ``(e [n_tok], top [B])`` where ``top[b]`` is the global index of
+    the prompt's largest weight (lowest index among ties).
+    """
+    if not alpha > 0:
+        raise ValueError("alpha must be positive")
+    S = np.asarray(S, dtype=np.float64)
+    H = np.asarray(H, dtype=np.float64)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    e = np.empty_like(S)
+    top = np.empty(len(cu) - 1, dtype=np.int64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        s, h = S[lo:hi], H[lo:hi]
+        if norm == "zscore":
+            s, h = _zscore(s), _zscore(h)
+        elif norm != "none":
+            raise ValueError(norm)
+        T = lambda1 * s + lambda2 * h
+        u = T / alpha
+        w = np.exp(u - u.max())
+        e[lo:hi] = w / w.sum()
+        top[b] = lo + int(np.argmax(e[lo:hi]))
+    return e, top
+
+
+# ----------------------------------------------------------------------------- Eq. 5
+
+def pool(X, e, cu_seqlens) -> np.ndarray:
+    """h = sum_i e_i h_i over each prompt's tokens (Eq. 5); returns [B, d]."""
+    Xd = widen(X)
+    e = np.asarray(e, dtype=np.float64)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    out = np.zeros((len(cu) - 1, Xd.shape[1]), dtype=np.float64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        out[b] = e[lo:hi] @ Xd[lo:hi]
+    return out
+
+
+# ----------------------------------------------------------------------------- length head, Eq. 7
+
+def _act(a: np.ndarray, act: str) -> np.ndarray:
+    if act == "relu":
+        return np.maximum(a, 0.0)
+    if act == "gelu_tanh":
+        return 0.5 * a * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (a + 0.044715 * a ** 3)))
+    raise ValueError(act)
+
+
+def predict(pooled, W1, b1, W2, b2, centres=None, act: str = "relu"):
+    """MLP length head on the pooled vectors.
+
+    ``o = W2 act(W1 h + b1) + b2``.  With one output (K = 1) y-hat is ``o``
+    (direct regression); with K > 1 bins, p-hat = softmax(o) and
+    y-hat = sum_k p-hat_k c_k (Eq. 7), and ``bin`` is the argmax of p-hat.
+    ``order`` lists the prompts by ascending y-hat, ties by index: the
+    shortest-job-first order of Section 5.4.
+    Returns ``(yhat [B], bin [B] or None, order [B])``.
+    """
+    h = np.asarray(pooled, dtype=np.float64)
+    W1 = np.asarray(W1, dtype=np.float64)
+    W2 = np.asarray(W2, dtype=np.float64)
+    b1 = np.zeros(W1.shape[0]) if b1 is None else np.asarray(b1, dtype=np.float64)
+    b2 = np.zeros(W2.shape[0]) if b2 is None else np.asarray(b2, dtype=np.float64)
+    a = _act(h @ W1.T + b1, act)
+    o = a @ W2.T + b2
+    K = W2.shape[0]
+    if K == 1:
+        yhat = o[:, 0]
+        bins = None
+    else:
+        c = np.asarray(centres, dtype=np.float64)
+        z = np.exp(o - o.max(axis=1, keepdims=True))
+        phat = z / z.sum(axis=1, keepdims=True)
+        yhat = phat @ c
+        bins = np.argmax(phat, axis=1)
+    order = np.argsort(yhat, kind="stable")
+    return yhat, bins, order
+
+
+# ----------------------------------------------------------------------------- Eq. 6, 8
+
+def soft_labels(i: int, K: int) -> np.ndarray:
+    """p_j = exp(-|j - i|) / sum_k exp(-|k - i|) over the K bins (Eq. 6)."""
+    j = np.arange(K)
+    w = np.exp(-np.abs(j - i).astype(np.float64))
+    return w / w.sum()
+
+
+def length_loss(p, phat, y, yhat, lambda3: float) -> float:
+    """lambda3 * CE(p, p-hat) + (1 - lambda3) * MSE(y, y-hat), batch means (Eq. 8)."""
+    p = np.asarray(p, dtype=np.float64)
+    phat = np.asarray(phat, dtype=np.float64)
+    ce = -(p * np.log(phat)).sum(axis=-1).mean()
+    mse = np.mean((np.asarray(y, dtype=np.float64) - np.asarray(yhat, dtype=np.float64)) ** 2)
+    return float(lambda3 * ce + (1.0 - lambda3) * mse)
+
+
+# ----------------------------------------------------------------------------- whole path
+
+def run_path(X, W, Q, K, cu_seqlens, lambda1: float, lambda2: float, alpha: float = 1.0,
+             norm: str = "none", head: Optional[Sequence] = None, act: str = "relu",
+             scale: Optional[float] = None):
+    """Entropy -> importance -> fused weights -> pooled vectors -> length head."""
+    H = token_entropy(X, W)
+    S = attn_importance(Q, K, cu_seqlens, scale)
+    e, top = combine_weights(S, H, cu_seqlens, lambda1, lambda2, alpha, norm)
+    h = pool(X, e, cu_seqlens)
+    out = {"H": H, "S": S, "e": e, "top": top, "pooled": h}
+    if head is not None:
+        W1, b1, W2, b2, centres = head
+        out["yhat"], out["bin"], out["order"] = predict(h, W1, b1, W2, b2, centres, act)
+    return out
