@@ -1,0 +1,224 @@
+#!/usr/bin/env python3
+"""Throughput of the ESTP scoring and pooling path on one MI355X.
+
+One step = the whole path over one batch: token entropy (fused LM-head GEMM),
+attention importance (two passes), fusion + pooling, length head + SJF order,
+enqueued back to back on one stream, inputs resident in HBM.  Prints one JSON
+line with prompt tokens/s, the roofline position of the dominant kernel
+(entropy GEMM, bf16 matrix cores) and the fp64 oracle timed on the host as a
+baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prompt tokens/sec scored+pooled on 1 MI355X; % bf16 MFMA peak; pooling HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def to_dev(a, torch):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(a).cuda()
+
+
+def cpu_baseline(w, inp, lam1, lam2, alpha, norm, entropy_rows: int):
+    """The fp64 oracle on a bounded sample of the workload: prompt 0 whole for importance,
+    fusion, pooling and the head; its first `entropy_rows` tokens for the entropy."""
+    import oracle
+    from synth import inputs as I
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    lengths = inp["lengths"]
+    N0 = int(lengths[0])
+    rows = np.arange(N0)
+    X0 = inp["X"][:N0]
+    t0 = time.perf_counter()
+    H0 = oracle.token_entropy(X0[:entropy_rows], inp["W"])
+    t_h = time.perf_counter() - t0
+    Q0 = inp["Q"][:, :N0]
+    K0 = inp["K"][:, :N0]
+    t0 = time.perf_counter()
+    S0 = oracle.attn_importance(Q0, K0, [0, N0])
+    t_s = time.perf_counter() - t0
+    Hfull = np.concatenate([H0, np.full(N0 - len(H0), float(np.mean(H0)))])
+    t0 = time.perf_counter()
+    e, _ = oracle.combine_weights(S0, Hfull, [0, N0], lam1, lam2, alpha, norm)
+    h = oracle.pool(X0, e, [0, N0])
+    oracle.predict(h, inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"])
+    t_p = time.perf_counter() - t0
+    per_tok = t_h / len(H0) + (t_s + t_p) / N0
+    del rows, I
+    return {
+        "value": 1.0 / per_tok,
+        "unit": "tokens/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": (f"prompt 0 of the workload ({N0} tokens) for importance, fusion, pooling and head; "
+                   f"its first {len(H0)} tokens for the entropy; per-token costs summed "
+                   f"(entropy {t_h:.1f} s, importance {t_s:.1f} s, rest {t_p:.2f} s)"),
+        "host_cpus": len(os.sched_getaffinity(0)),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama", help="synthetic workload preset (synth.workloads)")
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--lambda1", type=float, default=0.5)
+    ap.add_argument("--lambda2", type=float, default=0.5)
+    ap.add_argument("--alpha", type=float, default=1.0)
+    ap.add_argument("--norm", default="none", choices=["none", "zscore"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--entropy-sample-rows", type=int, default=512)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build targets one GPU: the path is measured on one MI355X; "
+                                   "run with --gpus 1 (multi-GPU sharding is described in DESIGN.md only)"}))
+        return 2
+
+    import torch
+
+    import paper_2608_15592_amd as estp
+    from paper_2608_15592_amd.path import alloc_buffers
+    import synth
+    from synth import inputs as I
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = synth.get_workload(args.workload)
+    log(f"workload {w.name}: {w.description}")
+    t0 = time.time()
+    inp = I.make_inputs(w, args.seed)
+    if w.dtype == "f32":
+        for k in ("X", "W", "Q", "K"):
+            inp[k] = I.f32_to_bf16_bits(inp[k])
+    n_tok = int(inp["n_tok"])
+    B = len(inp["lengths"])
+    max_len = int(inp["lengths"].max())
+    log(f"inputs drawn in {time.time() - t0:.1f} s: n_tok={n_tok}, B={B}, max_seqlen={max_len}")
+    t0 = time.time()
+    X, W, Q, K = (to_dev(inp[k], torch) for k in ("X", "W", "Q", "K"))
+    cu = to_dev(inp["cu_seqlens"], torch)
+    head = tuple(to_dev(inp[k], torch) for k in ("W1", "b1", "W2", "b2"))
+    Hdn, n_bins = w.head
+    torch.cuda.synchronize()
+    log(f"uploaded in {time.time() - t0:.1f} s")
+    bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, n_bins, X.device)
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        if evs:
+            evs[0].record(stream)
+        H = estp.token_entropy(X, W, H=bufs["H"], workspace=bufs["ws_entropy"], stream=stream)
+        if evs:
+            evs[1].record(stream)
+        S = estp.attn_importance(Q, K, cu, max_len, S=bufs["S"], workspace=bufs["ws_importance"], stream=stream)
+        if evs:
+            evs[2].record(stream)
+        pooled, _, _ = estp.combine_pool(X, S, H, cu, max_len, args.lambda1, args.lambda2, args.alpha, args.norm,
+                                         pooled=bufs["pooled"], e=bufs["e"], top=bufs["top"],
+                                         workspace=bufs["ws_pool"], stream=stream)
+        if evs:
+            evs[3].record(stream)
+        estp.predict(pooled, *head, None, workspace=bufs["ws_predict"], stream=stream)
+        if evs:
+            evs[4].record(stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+    per_call = np.array([[e[k].elapsed_time(e[k + 1]) for k in range(4)] for e in evs])
+    ent_ms, imp_ms, pool_ms, pred_ms = per_call.mean(axis=0)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step "
+        f"(entropy {ent_ms:.3f}, importance {imp_ms:.3f}, combine+pool {pool_ms:.3f}, head {pred_ms:.3f} ms)")
+
+    ent_flop = 2.0 * n_tok * w.V * w.d
+    imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
+    pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
+    ent_tflops = ent_flop / (ent_ms * 1e-3) / 1e12
+    pool_gbps = pool_bytes / (pool_ms * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": n_tok / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.description,
+            "n_tok": n_tok, "prompts": B, "d": w.d, "V": w.V, "Hq": w.Hq, "Hkv": w.Hkv, "dh": w.dh, "layers": w.L,
+            "lambda1": args.lambda1, "lambda2": args.lambda2, "alpha": args.alpha, "norm": args.norm,
+            "head": f"{w.d}->{Hdn}->{n_bins}",
+        },
+        "roofline": {
+            "kernel": "entropy_gemm_kernel (+ entropy_merge_kernel inside the timed call)",
+            "bound": "mfma",
+            "achieved": ent_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": ent_tflops / PEAK_BF16_TFLOPS,
+            "traffic": None,
+            "work_per_launch": f"2*n_tok*V*d = {ent_flop:.4g} FLOP",
+        },
+        "kernels_ms": {"token_entropy": ent_ms, "attn_importance": imp_ms, "combine_pool": pool_ms,
+                       "predict": pred_ms},
+        "importance": {"alg_flop": imp_flop_alg, "alg_tflops": imp_flop_alg / (imp_ms * 1e-3) / 1e12,
+                       "executed_tflops": 2 * imp_flop_alg / (imp_ms * 1e-3) / 1e12},
+        "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
+                    "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
+                    "note": "whole combine_pool call (weights + pooling + chunk reduction), warm after importance"},
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host sample ...")
+        result["cpu_baseline"] = cpu_baseline(w, inp, args.lambda1, args.lambda2, args.alpha, args.norm,
+                                              args.entropy_sample_rows)
+        log(f"oracle: {result['cpu_baseline']['value']:.1f} tokens/s")
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

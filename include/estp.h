@@ -1,0 +1,181 @@
+/*
+ * estp.h - C ABI of libestp, the MI355X (gfx950) library for the scoring and
+ * pooling path of ESTP, Entropy-and-Semantic Token Pooling (arXiv 2608.15592).
+ *
+ * ESTP predicts an LLM's output length from its prefill: every prompt token
+ * gets a next-token entropy H_i (Eq. 2, Section 4.2) and an attention-based
+ * semantic importance S_j (Eq. 1, Section 4.1); the two are fused into
+ * T_i = lambda1 S_i + lambda2 H_i (Eq. 3), turned into pooling weights by a
+ * temperature softmax over the prompt (Eq. 4), and the weighted sum of the
+ * hidden states (Eq. 5) feeds a small MLP length head whose K-bin
+ * distribution gives the expected length (Eq. 7, Section 4.3).  Predicted
+ * lengths order requests shortest-job-first (Section 5.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every tensor pointer is a DEVICE pointer (memory of the current HIP
+ *    device), contiguous, row-major, with the shapes given per call.  The
+ *    caller owns all memory; the library never allocates.  Scratch memory
+ *    comes from the caller through (workspace, workspace_bytes); the
+ *    matching *_workspace_size() call returns the bytes needed for a shape
+ *    (0 means none; a NULL workspace is then allowed).  Workspace pointers
+ *    must be 256-byte aligned.
+ *  - Inputs are read-only.  Outputs are fully overwritten (no pre-zeroing).
+ *  - Every call is asynchronous: it validates its arguments on the host,
+ *    enqueues its kernels on `stream` (a hipStream_t; NULL = the default
+ *    stream) and returns.  Results are visible after the caller synchronises
+ *    the stream.  Calls on one stream run in order.
+ *  - Argument validation happens before any device work: a failed check
+ *    returns an error and enqueues nothing.  Device-resident values
+ *    (cu_seqlens contents, NaN/Inf in tensors) are not inspected; a prompt of
+ *    length 0 or a cu_seqlens array that is not non-decreasing from 0 to
+ *    n_tok is invalid input with undefined results.  NaN/Inf propagate.
+ *  - Packed variable-length batches: prompt b owns tokens
+ *    [cu_seqlens[b], cu_seqlens[b+1]) of every [n_tok, ...] tensor;
+ *    cu_seqlens is int32 [B+1] in device memory with cu_seqlens[0] = 0 and
+ *    cu_seqlens[B] = n_tok; max_seqlen (host) bounds every prompt length.
+ *  - bf16 tensors hold IEEE bfloat16; arithmetic is fp32 throughout.
+ *  - The library keeps no global mutable state besides a per-thread error
+ *    message (estp_last_error); calls are thread-safe.
+ */
+#ifndef ESTP_H_
+#define ESTP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define ESTP_API __attribute__((visibility("default")))
+#else
+#define ESTP_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum estp_status {
+  ESTP_OK = 0,
+  ESTP_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad alignment, bad hyperparameter */
+  ESTP_ERR_UNSUPPORTED = 2, /* valid but not implemented (dtype, head_dim) */
+  ESTP_ERR_WORKSPACE = 3,   /* workspace smaller than *_workspace_size() */
+  ESTP_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} estp_status;
+
+typedef enum estp_dtype { ESTP_BF16 = 0, ESTP_F32 = 1 } estp_dtype;
+
+/* How S and H are scaled before Eq. 3.  NONE is Eq. 3 as printed; ZSCORE
+ * replaces S and H by their per-prompt z-scores (population standard
+ * deviation, (v - mean) / (std + 1e-6)) so that both terms are commensurate. */
+typedef enum estp_norm { ESTP_NORM_NONE = 0, ESTP_NORM_ZSCORE = 1 } estp_norm;
+
+/* Hidden activation of the length head (the paper names an MLP predictor
+ * without fixing its activation). */
+typedef enum estp_act { ESTP_ACT_RELU = 0, ESTP_ACT_GELU_TANH = 1 } estp_act;
+
+/* Library version, e.g. 100 for 0.1.0. */
+ESTP_API int estp_version(void);
+
+/* Static text for a status code. */
+ESTP_API const char* estp_status_string(int status);
+
+/* Detail of the last failed call on this thread ("" if none). */
+ESTP_API const char* estp_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Token entropy (Eq. 2, Section 4.2).
+ *
+ *   H[i] = - sum_v P_i(v) ln P_i(v),  P_i = softmax_v(z_i),  z_i = W x_i
+ *
+ * for every row i of X: the entropy, in nats, of the next-token distribution
+ * the LM head assigns from token i's final-layer hidden state.  The logits
+ * z_i (n_tok x V) never reach memory: a bf16 matrix-core GEMM streams the
+ * vocabulary and keeps a running max / exp-sum / sum(p*z) per row.
+ *
+ *   X  [n_tok, d]  hidden states (dtype), 16-byte aligned
+ *   W  [V, d]      LM-head weight in nn.Linear layout (dtype), 16-byte aligned
+ *   H  [n_tok]     float32 output
+ *   dtype          ESTP_BF16 (ESTP_F32 returns ESTP_ERR_UNSUPPORTED)
+ * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype);
+ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
+                       float* H, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Attention importance (Eq. 1, Section 4.1).
+ *
+ *   S[j] = sum_l (1/N_b) sum_{i>=j} (1/Hq) sum_h A^{l,h}_{ij}
+ *   A^{l,h}_{ij} = exp(scale q^{l,h}_i . k^{l,g(h)}_j) / sum_{j'<=i} exp(scale q^{l,h}_i . k^{l,g(h)}_{j'})
+ *
+ * for each token j of prompt b (N_b tokens): the mean over the prompt's
+ * queries of the causal attention it receives, averaged over the query heads,
+ * summed over the L layers given.  The diagonal A_jj is included.  Query head
+ * h reads key head g(h) = h / (Hq / Hkv).  The N x N attention never reaches
+ * memory: pass 1 records each query row's log-sum-exp, pass 2 re-forms the
+ * scores per key block and sums exp(s - lse) over the later queries.  Each
+ * prompt's S sums to L.
+ *
+ *   Q  [L, n_tok, Hq, dh]   post-RoPE queries (dtype), 16-byte aligned
+ *   K  [L, n_tok, Hkv, dh]  post-RoPE keys (dtype), 16-byte aligned
+ *   cu_seqlens [B+1]        int32, device
+ *   scale                   score scale, typically 1/sqrt(dh); finite, > 0
+ *   S  [n_tok]              float32 output
+ *   dtype                   ESTP_BF16
+ * Requires Hq % Hkv == 0, dh in {32, 64, 128}, 1 <= max_seqlen.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_attn_importance_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L, int32_t Hq,
+                                           int32_t Hkv, int32_t dh, int dtype);
+ESTP_API int estp_attn_importance(const void* Q, const void* K, const int32_t* cu_seqlens, int32_t B, int32_t max_seqlen,
+                         int64_t n_tok, int32_t L, int32_t Hq, int32_t Hkv, int32_t dh, float scale, int dtype,
+                         float* S, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Fusion and pooling (Eq. 3, Eq. 4, Eq. 5, Section 4.2).
+ *
+ *   T_i = lambda1 S_i + lambda2 H_i              (after `norm`, per prompt)
+ *   e_i = exp(T_i / alpha) / sum_{j in prompt} exp(T_j / alpha)
+ *   pooled[b] = sum_{i in prompt b} e_i x_i
+ *
+ *   X  [n_tok, d]    hidden states (dtype), 16-byte aligned
+ *   S, H [n_tok]     float32 scores (from the two calls above or any source)
+ *   alpha            temperature, finite, > 0
+ *   pooled [B, d]    float32 output
+ *   e   [n_tok]      float32 output of the weights, or NULL
+ *   top [B]          int32 output: global index of each prompt's largest
+ *                    weight (lowest index among equal maxima), or NULL
+ *   dtype            ESTP_BF16 or ESTP_F32
+ * Requires d >= 8, d % 8 == 0.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d, int dtype);
+ESTP_API int estp_combine_pool(const void* X, const float* S, const float* H, const int32_t* cu_seqlens, int32_t B,
+                      int32_t max_seqlen, int64_t n_tok, int32_t d, float lambda1, float lambda2, float alpha,
+                      int norm, int dtype, float* pooled, float* e, int32_t* top, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Length head (Section 4.3, Eq. 7) and shortest-job-first order (Section 5.4).
+ *
+ *   a = act(W1 pooled[b] + b1),   o = W2 a + b2
+ *   K == 1: yhat[b] = o[0]                               (direct regression)
+ *   K  > 1: p = softmax(o), yhat[b] = sum_k p_k centres[k], bin[b] = argmax_k p_k
+ *   order: prompt indices sorted by ascending yhat, ties by index
+ *
+ *   pooled [B, d]       float32
+ *   W1 [hidden, d], b1 [hidden] or NULL (zero), W2 [K, hidden], b2 [K] or NULL: float32
+ *   centres [K]         float32 bin centres (required when K > 1, ignored when K == 1)
+ *   yhat [B]            float32 output
+ *   bin  [B]            int32 output or NULL (written only when K > 1)
+ *   order [B]           int32 output or NULL
+ * Requires B >= 1, d >= 1, hidden >= 1, 1 <= K <= 1024, B <= 65536.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_predict_workspace_size(int32_t B, int32_t d, int32_t hidden, int32_t K);
+ESTP_API int estp_predict(const float* pooled, int32_t B, int32_t d, const float* W1, const float* b1, int32_t hidden,
+                 int act, const float* W2, const float* b2, int32_t K, const float* centres, float* yhat,
+                 int32_t* bin, int32_t* order, void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ESTP_H_ */

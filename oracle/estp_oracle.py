@@ -45,16 +45,18 @@ def widen(a) -> np.ndarray:
 
 # ----------------------------------------------------------------------------- Eq. 2
 
-def token_entropy(X, W, row_chunk: int = 64) -> np.ndarray:
+def token_entropy(X, W, row_chunk: Optional[int] = None) -> np.ndarray:
     """H_i = -sum_v P(v) log P(v), P = softmax over the vocabulary of W h_i (Eq. 2).
 
     ``X`` [n, d] hidden states, ``W`` [V, d] LM-head weight.  Rows are
-    processed ``row_chunk`` at a time only to bound memory; every row sees its
-    complete logit vector.
+    processed ``row_chunk`` at a time only to bound memory (default: about
+    512 MiB of logits per chunk); every row sees its complete logit vector.
     """
     Xd = widen(X)
     Wd = widen(W)
     n = Xd.shape[0]
+    if row_chunk is None:
+        row_chunk = int(max(64, min(1024, (1 << 26) // max(1, Wd.shape[0]))))
     H = np.empty(n, dtype=np.float64)
     for r0 in range(0, n, row_chunk):
         z = Xd[r0:r0 + row_chunk] @ Wd.T                      # logits, [rows, V]

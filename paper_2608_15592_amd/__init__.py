@@ -1,0 +1,24 @@
+"""ESTP scoring and pooling on MI355X (gfx950).
+
+Python face of libestp.so: the four calls of the ESTP path (arXiv 2608.15592)
+
+* ``token_entropy``   - Eq. 2, fused LM-head GEMM with streaming entropy
+* ``attn_importance`` - Eq. 1, two-pass causal attention column means
+* ``combine_pool``    - Eq. 3-5, temperature softmax of the fused score and weighted pooling
+* ``predict``         - length head (Section 4.3, Eq. 7) and shortest-job-first order
+
+plus ``run_path`` chaining them.  All computation runs in the library's HIP
+kernels; torch only supplies device memory and the stream.
+"""
+from ._lib import (  # noqa: F401
+    EXPORTS,
+    EstpError,
+    LIB_PATH,
+    attn_importance,
+    combine_pool,
+    load,
+    predict,
+    token_entropy,
+    token_entropy_workspace_size,
+)
+from .path import run_path  # noqa: F401

@@ -1,0 +1,242 @@
+"""ctypes binding of libestp (the C ABI in include/estp.h).
+
+Argument marshalling only: shapes and strides are read from torch tensors,
+outputs and workspaces are allocated with torch on the tensors' device, and
+every step of the computation runs in the library's HIP kernels on the
+current torch stream.  There is no fallback: if the library is missing or a
+call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libestp.so")
+
+ESTP_OK, ESTP_ERR_INVALID_ARG, ESTP_ERR_UNSUPPORTED, ESTP_ERR_WORKSPACE, ESTP_ERR_HIP = range(5)
+ESTP_BF16, ESTP_F32 = 0, 1
+NORMS = {"none": 0, "zscore": 1}
+ACTS = {"relu": 0, "gelu_tanh": 1}
+
+EXPORTS = (
+    "estp_version", "estp_status_string", "estp_last_error",
+    "estp_token_entropy_workspace_size", "estp_token_entropy",
+    "estp_attn_importance_workspace_size", "estp_attn_importance",
+    "estp_combine_pool_workspace_size", "estp_combine_pool",
+    "estp_predict_workspace_size", "estp_predict",
+)
+
+
+class EstpError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status}: {detail}")
+        self.status = status
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_SZ = ctypes.c_size_t
+_INT = ctypes.c_int
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libestp.so (built by ``paper_2608_15592_amd.build``) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_15592_amd.build`")
+    lib = ctypes.CDLL(path)
+    lib.estp_version.restype = _INT
+    lib.estp_version.argtypes = []
+    lib.estp_status_string.restype = ctypes.c_char_p
+    lib.estp_status_string.argtypes = [_INT]
+    lib.estp_last_error.restype = ctypes.c_char_p
+    lib.estp_last_error.argtypes = []
+    lib.estp_token_entropy_workspace_size.restype = _SZ
+    lib.estp_token_entropy_workspace_size.argtypes = [_I64, _I32, _I32, _INT]
+    lib.estp_token_entropy.restype = _INT
+    lib.estp_token_entropy.argtypes = [_P, _P, _I64, _I32, _I32, _INT, _P, _P, _SZ, _P]
+    lib.estp_attn_importance_workspace_size.restype = _SZ
+    lib.estp_attn_importance_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _I32, _I32, _I32, _INT]
+    lib.estp_attn_importance.restype = _INT
+    lib.estp_attn_importance.argtypes = [_P, _P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _I32, _F, _INT, _P, _P,
+                                         _SZ, _P]
+    lib.estp_combine_pool_workspace_size.restype = _SZ
+    lib.estp_combine_pool_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _INT]
+    lib.estp_combine_pool.restype = _INT
+    lib.estp_combine_pool.argtypes = [_P, _P, _P, _P, _I32, _I32, _I64, _I32, _F, _F, _F, _INT, _INT, _P, _P, _P,
+                                      _P, _SZ, _P]
+    lib.estp_predict_workspace_size.restype = _SZ
+    lib.estp_predict_workspace_size.argtypes = [_I32, _I32, _I32, _I32]
+    lib.estp_predict.restype = _INT
+    lib.estp_predict.argtypes = [_P, _I32, _I32, _P, _P, _I32, _INT, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ, _P]
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != ESTP_OK:
+        lib = load()
+        raise EstpError(status, where, lib.estp_last_error().decode())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return ESTP_BF16
+    if t.dtype == torch.float32:
+        return ESTP_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, device=None, dtype=None, ndim=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {t.dim()}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    if nbytes == 0:
+        return workspace, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+# ----------------------------------------------------------------------------- calls
+
+def token_entropy_workspace_size(n_tok: int, d: int, V: int, dtype=torch.bfloat16) -> int:
+    return load().estp_token_entropy_workspace_size(n_tok, d, V, ESTP_BF16 if dtype == torch.bfloat16 else ESTP_F32)
+
+
+def token_entropy(X: torch.Tensor, W: torch.Tensor, H: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """H[i] = entropy (nats) of softmax(W @ X[i]) over the vocabulary (Eq. 2)."""
+    lib = load()
+    _need(X, "X", ndim=2)
+    _need(W, "W", device=X.device, dtype=X.dtype, ndim=2)
+    n_tok, d = X.shape
+    V = W.shape[0]
+    if W.shape[1] != d:
+        raise ValueError("X and W disagree on d")
+    if H is None:
+        H = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+    _need(H, "H", device=X.device, dtype=torch.float32)
+    if H.numel() != n_tok:
+        raise ValueError("H must have n_tok elements")
+    dt = _dtype_code(X)
+    workspace, wsb = _workspace(lib.estp_token_entropy_workspace_size(n_tok, d, V, dt), X.device, workspace)
+    _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(workspace), wsb,
+                                  _stream(stream)), "estp_token_entropy")
+    return H
+
+
+def attn_importance(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, max_seqlen: int,
+                    scale: Optional[float] = None, S: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """S[j] = column mean of the head-averaged causal attention, summed over layers (Eq. 1).
+
+    Q [L, n_tok, Hq, dh], K [L, n_tok, Hkv, dh] (3-D tensors are one layer).
+    """
+    lib = load()
+    if Q.dim() == 3:
+        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
+    _need(Q, "Q", ndim=4)
+    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
+    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
+    L, n_tok, Hq, dh = Q.shape
+    Hkv = K.shape[2]
+    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
+        raise ValueError("Q and K shapes disagree")
+    B = cu_seqlens.numel() - 1
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    if S is None:
+        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+    _need(S, "S", device=Q.device, dtype=torch.float32)
+    dt = _dtype_code(Q)
+    ws = lib.estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
+    workspace, wsb = _workspace(ws, Q.device, workspace)
+    _check(lib.estp_attn_importance(_ptr(Q), _ptr(K), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L, Hq, Hkv, dh,
+                                    float(scale), dt, _ptr(S), _ptr(workspace), wsb, _stream(stream)),
+           "estp_attn_importance")
+    return S
+
+
+def combine_pool(X: torch.Tensor, S: torch.Tensor, H: torch.Tensor, cu_seqlens: torch.Tensor, max_seqlen: int,
+                 lambda1: float, lambda2: float, alpha: float = 1.0, norm: str = "none",
+                 pooled: Optional[torch.Tensor] = None, e: Optional[torch.Tensor] = None,
+                 top: Optional[torch.Tensor] = None, want_e: bool = True, want_top: bool = True,
+                 workspace: Optional[torch.Tensor] = None, stream=None):
+    """e = softmax over each prompt of (lambda1 S + lambda2 H) / alpha; pooled[b] = sum e_i X_i (Eq. 3-5).
+
+    Returns ``(pooled [B, d], e [n_tok] or None, top [B] or None)``.
+    """
+    lib = load()
+    _need(X, "X", ndim=2)
+    _need(S, "S", device=X.device, dtype=torch.float32)
+    _need(H, "H", device=X.device, dtype=torch.float32)
+    _need(cu_seqlens, "cu_seqlens", device=X.device, dtype=torch.int32, ndim=1)
+    n_tok, d = X.shape
+    B = cu_seqlens.numel() - 1
+    if pooled is None:
+        pooled = torch.empty(B, d, dtype=torch.float32, device=X.device)
+    if e is None and want_e:
+        e = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+    if top is None and want_top:
+        top = torch.empty(B, dtype=torch.int32, device=X.device)
+    dt = _dtype_code(X)
+    workspace, wsb = _workspace(lib.estp_combine_pool_workspace_size(n_tok, B, max_seqlen, d, dt), X.device,
+                                workspace)
+    _check(lib.estp_combine_pool(_ptr(X), _ptr(S), _ptr(H), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, d,
+                                 float(lambda1), float(lambda2), float(alpha), NORMS[norm], dt, _ptr(pooled), _ptr(e),
+                                 _ptr(top), _ptr(workspace), wsb, _stream(stream)), "estp_combine_pool")
+    return pooled, e, top
+
+
+def predict(pooled: torch.Tensor, W1: torch.Tensor, b1: Optional[torch.Tensor], W2: torch.Tensor,
+            b2: Optional[torch.Tensor], centres: Optional[torch.Tensor] = None, act: str = "relu",
+            want_order: bool = True, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Length head: returns ``(yhat [B], bin [B] or None, order [B] or None)`` (Section 4.3, Eq. 7)."""
+    lib = load()
+    _need(pooled, "pooled", dtype=torch.float32, ndim=2)
+    for t, n in ((W1, "W1"), (W2, "W2")):
+        _need(t, n, device=pooled.device, dtype=torch.float32, ndim=2)
+    B, d = pooled.shape
+    Hd, K = W1.shape[0], W2.shape[0]
+    if W1.shape[1] != d or W2.shape[1] != Hd:
+        raise ValueError("head weight shapes disagree")
+    yhat = torch.empty(B, dtype=torch.float32, device=pooled.device)
+    bins = torch.empty(B, dtype=torch.int32, device=pooled.device) if K > 1 else None
+    order = torch.empty(B, dtype=torch.int32, device=pooled.device) if want_order else None
+    workspace, wsb = _workspace(lib.estp_predict_workspace_size(B, d, Hd, K), pooled.device, workspace)
+    _check(lib.estp_predict(_ptr(pooled), B, d, _ptr(W1), _ptr(b1), Hd, ACTS[act], _ptr(W2), _ptr(b2), K,
+                            _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb,
+                            _stream(stream)), "estp_predict")
+    return yhat, bins, order

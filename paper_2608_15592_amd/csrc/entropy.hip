@@ -1,0 +1,361 @@
+// Token entropy, Eq. 2 (Section 4.2): H_i = -sum_v P_i(v) ln P_i(v) with
+// P_i = softmax(W x_i), fused into a bf16 matrix-core GEMM so the n_tok x V
+// logits never leave registers.
+//
+// Layout.  The GEMM is computed transposed, Z^T = W X^T: vocabulary rows are
+// the MFMA "M" side (A operand, rows of W) and tokens the "N" side (B operand,
+// rows of X).  Both operands are contiguous along the hidden dimension d, so
+// every 16-byte global load and every LDS fragment read is a contiguous run
+// of 8 bf16.  In the 32x32 MFMA output a lane owns one token column and 16
+// vocabulary rows, so the per-token reduction over the vocabulary runs in
+// registers with no cross-lane traffic until the very end.
+//
+// Work split.  A workgroup owns a 256-token tile and a strided subset of the
+// 256-row vocabulary tiles (vocab slice vs takes tiles vs, vs + n_vsplit, ...).
+// Its steps (vocabulary tile, hidden-depth stage) form one flat sequence that
+// an S-deep LDS ring prefetches straight from global memory
+// (global_load_lds_dwordx4, no register staging), across tile boundaries, so
+// the folding of a finished 256 x 256 tile into the running per-token state
+// (max, sum 2^(z2-m), sum 2^(z2-m)(z2-m), base-2 units) overlaps the loads of
+// the next tile.  The n_vsplit partial states per token are merged by a
+// second small kernel that writes H.  Workgroup ids are remapped so the 32
+// workgroups resident on one XCD (ids are dealt round-robin over the 8 XCDs)
+// cover 4 vocabulary slices x 8 token tiles, and one dispatch wave of 256
+// covers 16 x 16: concurrent workgroups stream the same W and X tiles through
+// that XCD's L2.
+#include "estp_common.h"
+
+namespace estp {
+namespace detail {
+
+constexpr int kBV = 256;       // vocabulary rows per tile
+constexpr int kBT = 256;       // tokens per tile
+constexpr int kThreads = 256;  // 4 waves: 2 (vocab) x 2 (tokens), 128 x 128 each
+constexpr int kMaxVsplit = 16;
+constexpr int kBK = 32;        // hidden-dimension depth per LDS stage
+constexpr int kStages = 4;     // LDS ring depth (prefetch distance kStages - 1)
+
+template <int BK>
+struct StageGeom {
+  static constexpr int kRowBytes = BK * 2;                  // bytes of one staged row
+  static constexpr int kChunks = kRowBytes / 16;            // 16-byte chunks per row
+  static constexpr int kRowsPerInst = 64 / kChunks;         // rows one wave instruction fills (1 KB)
+  static constexpr int kInstPerOperand = kBV / (kRowsPerInst * 4);  // per wave, per operand, per stage
+  static constexpr int kStageBytes = (kBV + kBT) * kRowBytes;
+  static constexpr int kRowsPerWindow = 256 / kRowBytes;    // rows per 256-byte bank window
+  // Chunk swizzle: rows that share a 256-byte bank window offset differ in
+  // (row / kRowsPerWindow), so XOR-ing the chunk with it spreads the 16 rows
+  // read by 16 consecutive lanes over 16 distinct 16-byte bank groups.
+  __device__ static __forceinline__ int swz(int row, int chunk) {
+    return chunk ^ ((row / kRowsPerWindow) & (kChunks - 1));
+  }
+};
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <int BK, int S>
+__global__ __launch_bounds__(kThreads, 1) void entropy_gemm_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
+    int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
+  using G = StageGeom<BK>;
+  constexpr int kKK = BK / 16;                      // MFMA k-steps per stage
+  constexpr int kLoadsPerStage = 2 * G::kInstPerOperand;  // vector-memory instructions per wave per stage
+  __shared__ __attribute__((aligned(16))) char lds[S * G::kStageBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wv = wave & 1;   // which 128-row half of the vocabulary tile
+  const int wt = wave >> 1;  // which 128-token half of the token tile
+
+  // ---- workgroup -> (vocabulary slice, token tile)
+  int vs, tt;
+  {
+    const int bid = blockIdx.x;
+    if (n_vsplit == 16 && (n_tt % 16) == 0) {
+      const int xcd = bid & 7, j = bid >> 3;
+      const int wave_idx = j >> 5, jj = j & 31;
+      vs = (xcd & 3) * 4 + (jj & 3);
+      tt = wave_idx * 16 + (xcd >> 2) * 8 + (jj >> 2);
+    } else {
+      vs = bid % n_vsplit;
+      tt = bid / n_vsplit;
+    }
+  }
+  const int nk = d / BK;
+  const int n_my_tiles = (n_vt - vs + n_vsplit - 1) / n_vsplit;
+  const int n_steps = n_my_tiles * nk;
+  const size_t row_stride = size_t(d) * 2;  // bytes per row of W and X
+
+  // ---- staging: lane l of instruction i fills row kRowsPerInst*(4 i + wave) + l / kChunks,
+  // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.
+  uint32_t offw[G::kInstPerOperand], offx[G::kInstPerOperand];
+  const char* xt = reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride;
+#pragma unroll
+  for (int i = 0; i < G::kInstPerOperand; ++i) {
+    const int row = G::kRowsPerInst * (4 * i + wave) + lane / G::kChunks;
+    const int chunk = G::swz(row, lane % G::kChunks);
+    const int tr = min(tt * kBT + row, n_tok - 1) - tt * kBT;
+    offx[i] = uint32_t(tr) * uint32_t(row_stride) + uint32_t(chunk * 16);
+  }
+  auto set_w_offsets = [&](int vt) {
+#pragma unroll
+    for (int i = 0; i < G::kInstPerOperand; ++i) {
+      const int row = G::kRowsPerInst * (4 * i + wave) + lane / G::kChunks;
+      const int chunk = G::swz(row, lane % G::kChunks);
+      const int vr = min(vt * kBV + row, V - 1) - vt * kBV;
+      offw[i] = uint32_t(vr) * uint32_t(row_stride) + uint32_t(chunk * 16);
+    }
+  };
+  auto issue_stage = [&](int vt, int ks, int slot) {
+    char* base = lds + slot * G::kStageBytes;
+    const char* wk = reinterpret_cast<const char*>(W) + size_t(vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
+    const char* xk = xt + size_t(ks) * G::kRowBytes;
+#pragma unroll
+    for (int i = 0; i < G::kInstPerOperand; ++i) {
+      char* dst = base + G::kRowsPerInst * (4 * i + wave) * G::kRowBytes;
+      lds_dma16(wk + offw[i], dst);
+      lds_dma16(xk + offx[i], dst + kBV * G::kRowBytes);
+    }
+  };
+
+  // ---- prefetch state: the step (tile index, depth stage) whose loads are issued next
+  int pf_tile = 0, pf_ks = 0, pf_step = 0;
+  set_w_offsets(vs);
+  auto issue_next = [&]() {
+    if (pf_step < n_steps) {
+      issue_stage(vs + pf_tile * n_vsplit, pf_ks, pf_step % S);
+      ++pf_step;
+      if (++pf_ks == nk) {
+        pf_ks = 0;
+        ++pf_tile;
+        if (pf_tile < n_my_tiles) set_w_offsets(vs + pf_tile * n_vsplit);
+      }
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p) issue_next();
+
+  // ---- per-lane entropy state for the 4 token columns this lane owns
+  Ent2 st[4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) st[cb] = Ent2{-INFINITY, 0.f, 0.f};
+
+  const int frag_row = lane & 31;
+  const int frag_half = lane >> 5;
+  int ra[4], rb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ra[i] = wv * 128 + i * 32 + frag_row;
+    rb[i] = wt * 128 + i * 32 + frag_row;
+  }
+
+  for (int tile = 0; tile < n_my_tiles; ++tile) {
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    for (int ks = 0; ks < nk; ++ks) {
+    const int step = tile * nk + ks;
+    // stage `step` must have landed (own loads), then be visible from every wave;
+    // the barrier also retires all reads of the slot the next prefetch overwrites.
+    if (n_steps - 1 - step >= S - 2) {
+      wait_vm<(S - 2) * kLoadsPerStage>();
+    } else {
+      wait_vm<0>();
+    }
+    __syncthreads();
+    issue_next();
+
+    const char* sa = lds + (step % S) * G::kStageBytes;
+    const char* sb = sa + kBV * G::kRowBytes;
+    bf16x8_t fa[2][4], fb[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      fa[0][i] = *reinterpret_cast<const bf16x8_t*>(sa + ra[i] * G::kRowBytes + G::swz(ra[i], frag_half) * 16);
+      fb[0][i] = *reinterpret_cast<const bf16x8_t*>(sb + rb[i] * G::kRowBytes + G::swz(rb[i], frag_half) * 16);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kKK; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < kKK) {
+        const int chunk = (kk + 1) * 2 + frag_half;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          fa[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t*>(sa + ra[i] * G::kRowBytes + G::swz(ra[i], chunk) * 16);
+          fb[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t*>(sb + rb[i] * G::kRowBytes + G::swz(rb[i], chunk) * 16);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+    }
+
+    }  // ks
+
+    {
+      // ---- fold the finished tile into the running states, one 32 x 32 block at a
+      // time.  acc[i][j][r] is the logit of vocabulary row
+      // vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4 for token
+      // tt*256 + wt*128 + j*32 + frag_row.
+      const int vt = vs + tile * n_vsplit;
+      const int vbase = vt * kBV + wv * 128 + 4 * frag_half;
+      const bool ragged = (vt + 1) * kBV > V;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        Ent2 e = st[j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float z[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            z[r] = acc[i][j][r];
+            if (ragged && vbase + i * 32 + 8 * (r >> 2) + (r & 3) >= V) z[r] = -INFINITY;
+          }
+          float mx = z[0];
+#pragma unroll
+          for (int r = 1; r < 16; ++r) mx = fmaxf(mx, z[r]);
+          const float mnew = fmaxf(e.m, mx * kLog2e);
+          const float dl = fmaxf(e.m - mnew, kExp2Floor);
+          const float f = fast_exp2(dl);
+          float s = f * e.s;
+          float t = f * (e.t + e.s * dl);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float dd = fmaxf(fmaf(z[r], kLog2e, -mnew), kExp2Floor);
+            const float p = fast_exp2(dd);
+            s += p;
+            t = fmaf(p, dd, t);
+          }
+          e = Ent2{mnew, s, t};
+        }
+        st[j] = e;
+      }
+    }
+  }  // tile
+
+  // ---- lanes l and l+32 hold the same tokens: merge them
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    Ent2 o;
+    o.m = __shfl_xor(st[j].m, 32, 64);
+    o.s = __shfl_xor(st[j].s, 32, 64);
+    o.t = __shfl_xor(st[j].t, 32, 64);
+    st[j] = ent2_merge(st[j], o);
+  }
+  // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS
+  __syncthreads();  // every wave is done reading the ring
+  float* xbuf = reinterpret_cast<float*>(lds);  // [2 (wt)][128 tokens][3]
+  if (wv == 1 && frag_half == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float* p = xbuf + (wt * 128 + j * 32 + frag_row) * 3;
+      p[0] = st[j].m;
+      p[1] = st[j].s;
+      p[2] = st[j].t;
+    }
+  }
+  __syncthreads();
+  if (wv == 0 && frag_half == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = wt * 128 + j * 32 + frag_row;
+      const float* p = xbuf + tl * 3;
+      Ent2 r = ent2_merge(st[j], Ent2{p[0], p[1], p[2]});
+      const int tok = tt * kBT + tl;
+      if (tok < n_tok) {
+        const size_t o = size_t(vs) * n_tok + tok;
+        part_m[o] = r.m;
+        part_s[o] = r.s;
+        part_t[o] = r.t;
+      }
+    }
+  }
+}
+
+// Merge the n_vsplit partial states of each token and write H in nats:
+// H = ln2 * (log2 s - t / s).
+__global__ __launch_bounds__(256) void entropy_merge_kernel(const float* __restrict__ part_m,
+                                                            const float* __restrict__ part_s,
+                                                            const float* __restrict__ part_t, int n_tok,
+                                                            int n_vsplit, float* __restrict__ H) {
+  const int tok = blockIdx.x * 256 + threadIdx.x;
+  if (tok >= n_tok) return;
+  Ent2 a{part_m[tok], part_s[tok], part_t[tok]};
+  for (int v = 1; v < n_vsplit; ++v) {
+    const size_t o = size_t(v) * n_tok + tok;
+    a = ent2_merge(a, Ent2{part_m[o], part_s[o], part_t[o]});
+  }
+  H[tok] = kLn2 * (fast_log2(a.s) - a.t / a.s);
+}
+
+int choose_vsplit(int n_vt) { return n_vt < kMaxVsplit ? n_vt : kMaxVsplit; }
+
+}  // namespace detail
+}  // namespace estp
+
+using namespace estp;
+using namespace estp::detail;
+
+extern "C" size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype) {
+  (void)d;
+  (void)dtype;
+  if (n_tok < 1 || V < 1) return 0;
+  const int n_vt = (V + kBV - 1) / kBV;
+  Carver c(nullptr);
+  for (int i = 0; i < 3; ++i) c.take<float>(size_t(choose_vsplit(n_vt)) * n_tok);
+  return c.bytes();
+}
+
+extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
+                                  float* H, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  ESTP_REQUIRE(X && W && H, ESTP_ERR_INVALID_ARG, "estp_token_entropy: X, W and H must be non-null");
+  ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: n_tok must be in [1, 2^31), got %lld", (long long)n_tok);
+  ESTP_REQUIRE(V >= 1, ESTP_ERR_INVALID_ARG, "estp_token_entropy: V must be >= 1, got %d", V);
+  ESTP_REQUIRE(d >= 8 && d % 8 == 0, ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: d must be a positive multiple of 8, got %d", d);
+  ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: unknown dtype %d", dtype);
+  ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED, "estp_token_entropy: only ESTP_BF16 inputs are supported");
+  ESTP_REQUIRE(d % kBK == 0, ESTP_ERR_UNSUPPORTED,
+               "estp_token_entropy: d must be a multiple of %d for the matrix-core path, got %d", kBK, d);
+  ESTP_REQUIRE(size_t(d) * 2 * kBV < (size_t(1) << 32), ESTP_ERR_UNSUPPORTED,
+               "estp_token_entropy: d = %d too large", d);
+  ESTP_REQUIRE(aligned(X, 16) && aligned(W, 16), ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: X and W must be 16-byte aligned");
+  const size_t need = estp_token_entropy_workspace_size(n_tok, d, V, dtype);
+  ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
+               "estp_token_entropy: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: workspace must be non-null and 256-byte aligned");
+
+  const int n = int(n_tok);
+  const int n_vt = (V + kBV - 1) / kBV;
+  const int n_tt = (n + kBT - 1) / kBT;
+  const int n_vsplit = choose_vsplit(n_vt);
+  Carver c(workspace);
+  float* pm = c.take<float>(size_t(n_vsplit) * n);
+  float* ps = c.take<float>(size_t(n_vsplit) * n);
+  float* pt = c.take<float>(size_t(n_vsplit) * n);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  entropy_gemm_kernel<kBK, kStages><<<dim3(n_vsplit * n_tt), dim3(kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+  ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
+  entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
+  ESTP_CHECK_LAUNCH("entropy_merge_kernel");
+  return ESTP_OK;
+}

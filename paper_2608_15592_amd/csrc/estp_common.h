@@ -1,0 +1,125 @@
+// Shared helpers of libestp: bf16 handling, exp2/log2, wave reductions, the
+// per-thread error message and workspace carving.  gfx950 (CDNA4) only:
+// wave64, matrix-core (MFMA) bf16 instructions with fp32 accumulation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "estp.h"
+
+namespace estp {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// Generic pointer into __shared__ memory -> LDS address-space pointer.
+__device__ __forceinline__ lds_ptr_t to_lds(void* p) { return (lds_ptr_t)(p); }
+
+// 16-byte global -> LDS transfer (global_load_lds_dwordx4): each lane of the
+// wave fetches 16 bytes from its own `src`; they land in LDS at
+// dst_wave_base + 16 * lane.  `dst_wave_base` must be uniform across the wave.
+// The builtin only exists in the device pass; the host pass (which only needs
+// the kernel's launch stub) sees an empty body.
+__device__ __forceinline__ void lds_dma16(const void* src, void* dst_wave_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, to_lds(dst_wave_base), 16, 0, 0);
+#endif
+}
+
+// Wait until every outstanding vector-memory load of this wave has landed,
+// including global -> LDS transfers (s_waitcnt vmcnt(0); other counters untouched).
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+// exp2 of anything below this is 0 in fp32; used to clamp (-inf) - (-inf) style cases.
+constexpr float kExp2Floor = -256.0f;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+
+// v_exp_f32 / v_log_f32: hardware base-2 exponential and logarithm.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Online-softmax state in base-2 units: m = running max of z*log2e,
+// s = sum 2^(z2 - m), t = sum 2^(z2 - m) * (z2 - m).
+struct Ent2 {
+  float m, s, t;
+};
+
+// Merge two states; exp2 arguments are clamped so -inf maxima (empty states)
+// contribute exactly nothing instead of NaN.
+__device__ __forceinline__ Ent2 ent2_merge(Ent2 a, Ent2 b) {
+  float M = fmaxf(a.m, b.m);
+  float da = fmaxf(a.m - M, kExp2Floor);
+  float db = fmaxf(b.m - M, kExp2Floor);
+  float fa = fast_exp2(da), fb = fast_exp2(db);
+  Ent2 r;
+  r.m = M;
+  r.s = fa * a.s + fb * b.s;
+  r.t = fa * (a.t + a.s * da) + fb * (b.t + b.s * db);
+  return r;
+}
+
+// ------------------------------------------------------------------ host side
+
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void clear_error();
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Sequential carving of a caller workspace into 256-byte aligned pieces.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = align_up(off, 256);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t bytes() const { return align_up(off, 256); }
+};
+
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace estp
+
+#define ESTP_REQUIRE(cond, code, ...)  \
+  do {                                 \
+    if (!(cond)) {                     \
+      ::estp::set_error(__VA_ARGS__);  \
+      return (code);                   \
+    }                                  \
+  } while (0)
+
+#define ESTP_CHECK_LAUNCH(what)                                                          \
+  do {                                                                                   \
+    hipError_t e_ = hipGetLastError();                                                   \
+    if (e_ != hipSuccess) {                                                              \
+      ::estp::set_error("%s: %s", (what), hipGetErrorString(e_));                        \
+      return ESTP_ERR_HIP;                                                               \
+    }                                                                                    \
+  } while (0)

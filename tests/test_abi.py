@@ -1,0 +1,157 @@
+"""The C ABI library: it loads, exports every symbol include/estp.h declares, and rejects
+invalid arguments on the host before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_15592_amd as estp
+from paper_2608_15592_amd import _lib
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "estp.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"ESTP_API\s+[\w\s\*]+?\b(estp_\w+)\s*\(", txt)))
+
+
+def test_header_declares_expected_calls():
+    names = _declared()
+    for n in ("estp_token_entropy", "estp_attn_importance", "estp_combine_pool", "estp_predict"):
+        assert n in names
+    assert set(names) == set(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = estp.load()
+    for n in _declared():
+        assert hasattr(lib, n), n
+    assert lib.estp_version() >= 100
+    for code in range(5):
+        assert lib.estp_status_string(code).startswith(b"ESTP_")
+
+
+def _gpu_present():
+    import torch
+    return torch.cuda.is_available()
+
+
+# Every case below fails host-side validation; they run only where no GPU is visible, so
+# that the fake (aligned, non-null) pointers can never reach a kernel.
+needs_no_gpu = pytest.mark.skipif(_gpu_present(), reason="host-validation cases use fake pointers")
+
+FAKE = ctypes.c_void_p(1 << 20)
+UNALIGNED = ctypes.c_void_p((1 << 20) + 2)
+WS = ctypes.c_void_p(1 << 24)
+
+
+@needs_no_gpu
+def test_entropy_validation():
+    lib = estp.load()
+    ws = lib.estp_token_entropy_workspace_size(100, 64, 1000, 0)
+    assert ws > 0
+    cases = [
+        ((None, FAKE, 100, 64, 1000, 0, FAKE, WS, ws, None), 1),        # null X
+        ((FAKE, FAKE, 0, 64, 1000, 0, FAKE, WS, ws, None), 1),          # n_tok < 1
+        ((FAKE, FAKE, 100, 60, 1000, 0, FAKE, WS, ws, None), 1),        # d % 8
+        ((FAKE, FAKE, 100, 64, 0, 0, FAKE, WS, ws, None), 1),           # V < 1
+        ((FAKE, FAKE, 100, 64, 1000, 7, FAKE, WS, ws, None), 1),        # unknown dtype
+        ((FAKE, FAKE, 100, 64, 1000, 1, FAKE, WS, ws, None), 2),        # f32 unsupported
+        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, WS, ws, None), 2),        # d not a multiple of 32
+        ((UNALIGNED, FAKE, 100, 64, 1000, 0, FAKE, WS, ws, None), 1),   # alignment
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, WS, ws - 1, None), 3),    # workspace short
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, None, ws, None), 1),      # workspace null
+    ]
+    for args, code in cases:
+        assert lib.estp_token_entropy(*args) == code, (args, lib.estp_last_error())
+        assert lib.estp_last_error()
+
+
+@needs_no_gpu
+def test_importance_validation():
+    lib = estp.load()
+    ws = lib.estp_attn_importance_workspace_size(100, 2, 60, 1, 4, 2, 64, 0)
+    base = [FAKE, FAKE, FAKE, 2, 60, 100, 1, 4, 2, 64, 0.125, 0, FAKE, WS, ws, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"Q": 0, "B": 3, "max_seqlen": 4, "n_tok": 5, "L": 6, "Hq": 7, "Hkv": 8, "dh": 9, "scale": 10,
+               "dtype": 11, "S": 12, "ws": 13, "wsb": 14}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_attn_importance(*a)
+
+    assert call(Q=None) == 1
+    assert call(B=0) == 1
+    assert call(Hq=5) == 1                # Hq % Hkv
+    assert call(scale=0.0) == 1
+    assert call(scale=float("inf")) == 1
+    assert call(max_seqlen=101) == 1      # longer than n_tok
+    assert call(dh=96) == 2
+    assert call(dtype=1) == 2
+    assert call(wsb=ws - 1) == 3
+    assert call(Q=UNALIGNED) == 1
+
+
+@needs_no_gpu
+def test_combine_pool_validation():
+    lib = estp.load()
+    ws = lib.estp_combine_pool_workspace_size(100, 2, 60, 64, 0)
+    base = [FAKE, FAKE, FAKE, FAKE, 2, 60, 100, 64, 0.5, 0.5, 1.0, 0, 0, FAKE, None, None, WS, ws, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"X": 0, "d": 7, "l1": 8, "alpha": 10, "norm": 11, "dtype": 12, "pooled": 13, "wsb": 17}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_combine_pool(*a)
+
+    assert call(X=None) == 1
+    assert call(pooled=None) == 1
+    assert call(d=12) == 1
+    assert call(alpha=0.0) == 1
+    assert call(alpha=-1.0) == 1
+    assert call(alpha=float("nan")) == 1
+    assert call(l1=float("nan")) == 1
+    assert call(norm=5) == 1
+    assert call(dtype=3) == 1
+    assert call(wsb=ws - 1) == 3
+
+
+@needs_no_gpu
+def test_predict_validation():
+    lib = estp.load()
+    ws = lib.estp_predict_workspace_size(4, 64, 32, 8)
+    base = [FAKE, 4, 64, FAKE, None, 32, 0, FAKE, None, 8, FAKE, FAKE, None, None, WS, ws, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"pooled": 0, "B": 1, "act": 6, "K": 9, "centres": 10, "wsb": 15}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_predict(*a)
+
+    assert call(pooled=None) == 1
+    assert call(B=0) == 1
+    assert call(B=70000) == 1
+    assert call(K=2000) == 1
+    assert call(centres=None) == 1      # K > 1 needs centres
+    assert call(act=9) == 1
+    assert call(wsb=ws - 1) == 3
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError):
+        _lib.load.__wrapped__(str(tmp_path / "missing.so")) if hasattr(_lib.load, "__wrapped__") else \
+            _load_fresh(str(tmp_path / "missing.so"))
+
+
+def _load_fresh(path):
+    saved = _lib._lib
+    try:
+        _lib._lib = None
+        return _lib.load(path)
+    finally:
+        _lib._lib = saved

@@ -1,0 +1,246 @@
+"""HIP path vs the fp64 oracle, element by element, through the C ABI.
+
+Tolerances (fixed by the targets of the path): entropy |dH| <= 2e-3 nats;
+importance |dS| <= 1e-3 S + 1e-12; pooled vectors relative L2 <= 1e-3 per
+prompt; length head relative 1e-3; indices exact outside near ties (margin
+rule, see tests/_util.py).  Inputs are bf16 (the oracle widens the same bits).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_15592_amd as estp
+import synth
+from synth import inputs as I
+from tests._util import check_argmax_margin, check_order_margin, dev, host, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+H_TOL = 2e-3
+S_RTOL = 1e-3
+POOL_RTOL = 1e-3
+
+
+def _bf16(a):
+    return I.f32_to_bf16_bits(np.asarray(a, dtype=np.float32))
+
+
+def _hidden(n, d, seed, scale=1.0):
+    g = np.random.default_rng(seed)
+    z = g.standard_normal((n, d)).astype(np.float32)
+    z /= np.sqrt((z * z).mean(axis=1, keepdims=True))
+    return _bf16(z * scale)
+
+
+def _weight(V, d, seed, std=0.02):
+    g = np.random.default_rng(seed)
+    return _bf16(g.standard_normal((V, d)).astype(np.float32) * std)
+
+
+# ------------------------------------------------------------------------------------------ entropy
+
+ENTROPY_CASES = [
+    # (n_tok, d, V, W std, tag)
+    (128, 64, 1000, 0.02, "tiny-shape"),
+    (1, 64, 7, 0.02, "one-token-seven-words"),
+    (300, 128, 2500, 0.02, "ragged-tokens-and-vocab"),
+    (513, 1536, 4099, 0.02, "qwen-width-ragged"),
+    (256, 4096, 32768, 0.02, "llama-width-16-slices"),
+    (200, 256, 3000, 1.5, "sharp-logits"),
+    (64, 128, 600, 0.0, "uniform-logits"),
+]
+
+
+@pytest.mark.parametrize("n_tok,d,V,std,tag", ENTROPY_CASES, ids=[c[-1] for c in ENTROPY_CASES])
+def test_entropy_parity(n_tok, d, V, std, tag):
+    X = _hidden(n_tok, d, 1)
+    W = _weight(V, d, 2, std)
+    H = host(estp.token_entropy(dev(X), dev(W)))
+    ref = oracle.token_entropy(X, W)
+    err = np.abs(H - ref).max()
+    print(f"{tag}: max |dH| = {err:.3e} nats (H in [{ref.min():.3f}, {ref.max():.3f}])")
+    assert err <= H_TOL
+    if std == 0.0:
+        np.testing.assert_allclose(H, math.log(V), atol=H_TOL)
+
+
+def test_entropy_repeatable_bitwise():
+    X = dev(_hidden(700, 256, 3))
+    W = dev(_weight(5000, 256, 4))
+    a = estp.token_entropy(X, W).clone()
+    b = estp.token_entropy(X, W)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_entropy_rejects_f32():
+    X = torch.zeros(4, 64, device="cuda")
+    W = torch.zeros(10, 64, device="cuda")
+    with pytest.raises(estp.EstpError) as ei:
+        estp.token_entropy(X, W)
+    assert ei.value.status == 2
+
+
+# ------------------------------------------------------------------------------------------ importance
+
+IMPORTANCE_CASES = [
+    # (lengths, L, Hq, Hkv, dh, q scale, tag)
+    ([128], 1, 2, 2, 32, 1.0, "tiny-shape"),
+    ([1, 5, 31, 32, 33, 64, 65, 130, 257], 2, 4, 2, 64, 1.0, "varlen-ragged-gqa2"),
+    ([100, 300], 1, 12, 2, 128, 1.0, "qwen-heads-gqa6"),
+    ([200, 77], 2, 8, 2, 128, 6.0, "sharp-attention"),
+    ([1], 3, 2, 1, 32, 1.0, "single-token"),
+]
+
+
+def _qk(lengths, L, Hq, Hkv, dh, qscale, seed):
+    g = np.random.default_rng(seed)
+    n = sum(lengths)
+    hs = g.uniform(0.5, 2.0, size=(L, 1, Hq, 1)).astype(np.float32)
+    Q = _bf16(g.standard_normal((L, n, Hq, dh)).astype(np.float32) * hs * qscale)
+    K = _bf16(g.standard_normal((L, n, Hkv, dh)).astype(np.float32))
+    cu = I.cu_seqlens_from_lengths(lengths)
+    return Q, K, cu
+
+
+@pytest.mark.parametrize("lengths,L,Hq,Hkv,dh,qs,tag", IMPORTANCE_CASES, ids=[c[-1] for c in IMPORTANCE_CASES])
+def test_importance_parity(lengths, L, Hq, Hkv, dh, qs, tag):
+    Q, K, cu = _qk(lengths, L, Hq, Hkv, dh, qs, 5)
+    S = host(estp.attn_importance(dev(Q), dev(K), dev(cu), max(lengths)))
+    ref = oracle.attn_importance(Q, K, cu)
+    rel = np.abs(S - ref) / ref
+    print(f"{tag}: max rel |dS| = {rel.max():.3e}")
+    assert np.all(np.abs(S - ref) <= S_RTOL * ref + 1e-12)
+    for b in range(len(lengths)):
+        assert abs(S[cu[b]:cu[b + 1]].sum() - L) <= 1e-4 * L
+
+
+def test_importance_repeatable_bitwise():
+    Q, K, cu = _qk([300, 45, 600], 2, 8, 2, 128, 1.0, 6)
+    Qd, Kd, cud = dev(Q), dev(K), dev(cu)
+    a = estp.attn_importance(Qd, Kd, cud, 600).clone()
+    b = estp.attn_importance(Qd, Kd, cud, 600)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------------------------------------ combine + pool
+
+COMBINE_GRID = [(0.1, 0.9, 1.0), (0.5, 0.5, 0.5), (0.9, 0.1, 2.0), (0.0, 0.0, 1.0), (1.0, 0.0, 1.0), (0.0, 1.0, 0.5)]
+
+
+@pytest.mark.parametrize("xdtype", ["bf16", "f32"])
+@pytest.mark.parametrize("norm", ["none", "zscore"])
+def test_combine_pool_parity(xdtype, norm):
+    lengths = [1, 7, 256, 257, 600, 33]
+    n = sum(lengths)
+    d = 520
+    g = np.random.default_rng(7)
+    Xf = g.standard_normal((n, d)).astype(np.float32)
+    X = _bf16(Xf) if xdtype == "bf16" else Xf
+    S = (g.random(n) / 50).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    Xd, Sd, Hd, cud = dev(X), dev(S), dev(Hh), dev(cu)
+    ties = 0
+    for l1, l2, a in COMBINE_GRID:
+        pooled, e, top = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
+        e_ref, top_ref = oracle.combine_weights(S, Hh, cu, l1, l2, a, norm)
+        p_ref = oracle.pool(X, e_ref, cu)
+        np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+        P = host(pooled)
+        top = host(top)
+        for b in range(len(lengths)):
+            assert rel_l2(P[b], p_ref[b]) <= POOL_RTOL
+            lo, hi = cu[b], cu[b + 1]
+            res = check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
+            ties += res == "tie"
+    print(f"{xdtype}/{norm}: near-tie top groups seen: {ties}")
+
+
+def test_combine_pool_special_cases():
+    # lambda = 0 -> average pooling; identical rows pool to that row
+    lengths = [5, 300]
+    n = sum(lengths)
+    g = np.random.default_rng(8)
+    X = _bf16(g.standard_normal((n, 64)))
+    cu = I.cu_seqlens_from_lengths(lengths)
+    S = g.random(n).astype(np.float32)
+    H = g.random(n).astype(np.float32)
+    pooled, e, _ = estp.combine_pool(dev(X), dev(S), dev(H), dev(cu), 300, 0.0, 0.0, 1.0)
+    Xw = oracle.widen(X)
+    for b in range(2):
+        np.testing.assert_allclose(host(e)[cu[b]:cu[b + 1]], 1.0 / lengths[b], rtol=1e-6)
+        assert rel_l2(host(pooled)[b], Xw[cu[b]:cu[b + 1]].mean(0)) <= 1e-5
+    Xs = np.tile(X[:1], (n, 1))
+    pooled, _, _ = estp.combine_pool(dev(Xs), dev(S), dev(H), dev(cu), 300, 0.7, 0.3, 0.5)
+    for b in range(2):
+        assert rel_l2(host(pooled)[b], Xw[0]) <= 1e-6
+
+
+# ------------------------------------------------------------------------------------------ length head
+
+@pytest.mark.parametrize("K,act", [(1, "relu"), (8, "relu"), (8, "gelu_tanh"), (1, "gelu_tanh")])
+def test_predict_parity(K, act):
+    B, d, Hdn = 37, 256, 96
+    g = np.random.default_rng(9)
+    P = g.standard_normal((B, d)).astype(np.float32)
+    W1 = (g.standard_normal((Hdn, d)) * 0.1).astype(np.float32)
+    b1 = (g.standard_normal(Hdn) * 0.1).astype(np.float32)
+    W2 = (g.standard_normal((K, Hdn)) * 0.3).astype(np.float32)
+    b2 = (g.standard_normal(K) * 0.1).astype(np.float32)
+    c = np.linspace(50, 3000, K).astype(np.float32)
+    y, bins, order = estp.predict(dev(P), dev(W1), dev(b1), dev(W2), dev(b2), dev(c) if K > 1 else None, act)
+    y_ref, bin_ref, order_ref = oracle.predict(P, W1, b1, W2, b2, c, act)
+    y = host(y)
+    np.testing.assert_allclose(y, y_ref, rtol=1e-3, atol=1e-5)
+    delta = 4e-3 * np.abs(y_ref) + 4e-5
+    ties = check_order_margin(host(order), y_ref, delta)
+    if K > 1:
+        h = np.asarray(P, np.float64)
+        a = h @ W1.T + b1
+        a = np.maximum(a, 0) if act == "relu" else 0.5 * a * (1 + np.tanh(math.sqrt(2 / math.pi) * (a + 0.044715 * a ** 3)))
+        o = a @ W2.T + b2
+        for b in range(B):
+            check_argmax_margin(int(host(bins)[b]), o[b], 4e-3 * np.abs(o[b]).max())
+    print(f"K={K} {act}: max rel dy = {np.max(np.abs(y - y_ref) / np.abs(y_ref)):.2e}, near-tie order pairs {ties}")
+
+
+# ------------------------------------------------------------------------------------------ whole path
+
+def _run_both(w, seed=42, lam=(0.5, 0.5), alpha=1.0, norm="none"):
+    inp = I.make_inputs(w, seed)
+    if w.dtype == "f32":  # the matrix-core kernels take bf16: round once, both sides see the same bits
+        for k in ("X", "W", "Q", "K"):
+            inp[k] = I.f32_to_bf16_bits(inp[k])
+    cu = inp["cu_seqlens"]
+    head = (inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"])
+    out = estp.run_path(dev(inp["X"]), dev(inp["W"]), dev(inp["Q"]), dev(inp["K"]), dev(cu), int(inp["lengths"].max()),
+                        lam[0], lam[1], alpha, norm, head=tuple(dev(t) for t in head[:4]) + (None,))
+    ref = oracle.run_path(inp["X"], inp["W"], inp["Q"], inp["K"], cu, lam[0], lam[1], alpha, norm, head=head)
+    return {k: (host(v) if isinstance(v, torch.Tensor) else v) for k, v in out.items()}, ref, cu
+
+
+def test_full_path_tiny():
+    w = synth.get_workload("tiny")
+    got, ref, cu = _run_both(w)
+    assert np.abs(got["H"] - ref["H"]).max() <= H_TOL
+    assert np.all(np.abs(got["S"] - ref["S"]) <= S_RTOL * ref["S"] + 1e-12)
+    assert rel_l2(got["pooled"][0], ref["pooled"][0]) <= POOL_RTOL
+    np.testing.assert_allclose(got["yhat"], ref["yhat"], rtol=1e-3, atol=1e-6)
+    assert list(got["order"]) == list(ref["order"])
+    print(f"tiny: |dH| {np.abs(got['H'] - ref['H']).max():.2e}, rel dS "
+          f"{(np.abs(got['S'] - ref['S']) / ref['S']).max():.2e}, pooled rel {rel_l2(got['pooled'], ref['pooled']):.2e}")
+
+
+def test_full_path_qwen_shaped_small():
+    # Qwen2.5-1.5B widths and vocabulary (d=1536, V=151936, 12/2 heads of 128), 3 short prompts
+    w = synth.get_workload("qwen", n_prompts=3, seq_len=40)
+    got, ref, cu = _run_both(w, lam=(0.9, 0.1), alpha=0.5, norm="zscore")
+    assert np.abs(got["H"] - ref["H"]).max() <= H_TOL
+    assert np.all(np.abs(got["S"] - ref["S"]) <= S_RTOL * ref["S"] + 1e-12)
+    for b in range(3):
+        assert rel_l2(got["pooled"][b], ref["pooled"][b]) <= POOL_RTOL
