@@ -93,6 +93,8 @@ def main() -> int:
     ap.add_argument("--norm", default="none", choices=["none", "zscore"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--entropy-sample-rows", type=int, default=512)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run 3 device-to-device copies of BYTES (calibrates HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -109,6 +111,14 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        a = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe, "copies": 3}), flush=True)
+        return 0
     w = synth.get_workload(args.workload)
     log(f"workload {w.name}: {w.description}")
     t0 = time.time()
