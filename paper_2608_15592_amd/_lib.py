@@ -16,7 +16,7 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libestp.so")
+LIB_PATH = os.environ.get("ESTP_LIBRARY") or os.path.join(_HERE, "libestp.so")
 
 ESTP_OK, ESTP_ERR_INVALID_ARG, ESTP_ERR_UNSUPPORTED, ESTP_ERR_WORKSPACE, ESTP_ERR_HIP = range(5)
 ESTP_BF16, ESTP_F32 = 0, 1

@@ -30,49 +30,60 @@ namespace detail {
 
 constexpr int kBV = 256;       // vocabulary rows per tile
 constexpr int kBT = 256;       // tokens per tile
-constexpr int kThreads = 256;  // 4 waves: 2 (vocab) x 2 (tokens), 128 x 128 each
 constexpr int kMaxVsplit = 16;
-constexpr int kBK = 32;        // hidden-dimension depth per LDS stage
-constexpr int kStages = 4;     // LDS ring depth (prefetch distance kStages - 1)
+constexpr int kBK = 32;        // hidden-dimension depth per LDS stage: two 16-deep MFMA steps
+#ifndef ESTP_ENTROPY_STAGES
+#define ESTP_ENTROPY_STAGES 4
+#endif
+#ifndef ESTP_ENTROPY_WAVES
+#define ESTP_ENTROPY_WAVES 8
+#endif
+constexpr int kStages = ESTP_ENTROPY_STAGES;  // LDS ring depth
+constexpr int kWaves = ESTP_ENTROPY_WAVES;    // 4 (one per SIMD) or 8 (two per SIMD)
 
-template <int BK>
-struct StageGeom {
-  static constexpr int kRowBytes = BK * 2;                  // bytes of one staged row
-  static constexpr int kChunks = kRowBytes / 16;            // 16-byte chunks per row
-  static constexpr int kRowsPerInst = 64 / kChunks;         // rows one wave instruction fills (1 KB)
-  static constexpr int kInstPerOperand = kBV / (kRowsPerInst * 4);  // per wave, per operand, per stage
-  static constexpr int kStageBytes = (kBV + kBT) * kRowBytes;
-  static constexpr int kRowsPerWindow = 256 / kRowBytes;    // rows per 256-byte bank window
-  // Chunk swizzle: rows that share a 256-byte bank window offset differ in
-  // (row / kRowsPerWindow), so XOR-ing the chunk with it spreads the 16 rows
-  // read by 16 consecutive lanes over 16 distinct 16-byte bank groups.
+// Geometry of one LDS stage (kBV rows of W then kBT rows of X, kBK bf16 each)
+// and of the wave layout: waves split the 256 x 256 tile 2 (vocabulary) x
+// NW/2 (tokens); a wave owns 128 vocabulary rows x TW tokens.
+template <int NW>
+struct Geom {
+  static constexpr int kThreads = NW * 64;
+  static constexpr int TW = 2 * kBT / NW;                           // tokens per wave: 128 or 64
+  static constexpr int JT = TW / 32;                                // 32-token MFMA blocks per wave
+  static constexpr int kRowBytes = kBK * 2;                         // 64 B
+  static constexpr int kChunks = kRowBytes / 16;                    // 4 chunks of 16 B
+  static constexpr int kRowsPerInst = 64 / kChunks;                 // 16 rows per wave instruction (1 KB)
+  static constexpr int kInstPerOperand = kBV / (kRowsPerInst * NW); // per wave per operand per stage
+  static constexpr int kLoadsPerStage = 2 * kInstPerOperand;        // vector-memory instructions per wave
+  static constexpr int kStageBytes = (kBV + kBT) * kRowBytes;       // 32 KB
+  static constexpr int kRowsPerWindow = 256 / kRowBytes;            // 4 rows share a 256-byte bank window
+  // Chunk swizzle: the 16 rows that 16 consecutive lanes read at one logical
+  // chunk land in 16 distinct 16-byte bank groups.
   __device__ static __forceinline__ int swz(int row, int chunk) {
     return chunk ^ ((row / kRowsPerWindow) & (kChunks - 1));
   }
 };
 
-// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
-// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
-}
+// One 16-deep k step of a wave's tile: 4 A fragments (vocabulary rows) and
+// JT B fragments (tokens), 8 bf16 each.
+template <int JT>
+struct Frags {
+  bf16x8_t a[4], b[JT];
+};
 
-template <int BK, int S>
-__global__ __launch_bounds__(kThreads, 1) void entropy_gemm_kernel(
+template <int S, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
     int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
-  using G = StageGeom<BK>;
-  constexpr int kKK = BK / 16;                      // MFMA k-steps per stage
-  constexpr int kLoadsPerStage = 2 * G::kInstPerOperand;  // vector-memory instructions per wave per stage
+  using G = Geom<NW>;
+  constexpr int JT = G::JT;
+  static_assert(S >= 3, "the ring needs at least three stages");
   __shared__ __attribute__((aligned(16))) char lds[S * G::kStageBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave & 1;   // which 128-row half of the vocabulary tile
-  const int wt = wave >> 1;  // which 128-token half of the token tile
+  const int wt = wave >> 1;  // which TW-token slice of the token tile
 
   // ---- workgroup -> (vocabulary slice, token tile)
   int vs, tt;
@@ -88,167 +99,183 @@ __global__ __launch_bounds__(kThreads, 1) void entropy_gemm_kernel(
       tt = bid / n_vsplit;
     }
   }
-  const int nk = d / BK;
+  const int nk = d / kBK;
   const int n_my_tiles = (n_vt - vs + n_vsplit - 1) / n_vsplit;
   const int n_steps = n_my_tiles * nk;
   const size_t row_stride = size_t(d) * 2;  // bytes per row of W and X
 
-  // ---- staging: lane l of instruction i fills row kRowsPerInst*(4 i + wave) + l / kChunks,
+  // ---- staging: lane l of instruction i fills row kRowsPerInst*(NW i + wave) + l / kChunks,
   // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.
-  uint32_t offw[G::kInstPerOperand], offx[G::kInstPerOperand];
+  int st_row[G::kInstPerOperand];
+  uint32_t st_chunk_off[G::kInstPerOperand], offx[G::kInstPerOperand];
   const char* xt = reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride;
 #pragma unroll
   for (int i = 0; i < G::kInstPerOperand; ++i) {
-    const int row = G::kRowsPerInst * (4 * i + wave) + lane / G::kChunks;
-    const int chunk = G::swz(row, lane % G::kChunks);
-    const int tr = min(tt * kBT + row, n_tok - 1) - tt * kBT;
-    offx[i] = uint32_t(tr) * uint32_t(row_stride) + uint32_t(chunk * 16);
+    st_row[i] = G::kRowsPerInst * (NW * i + wave) + lane / G::kChunks;
+    st_chunk_off[i] = uint32_t(G::swz(st_row[i], lane % G::kChunks) * 16);
+    const int tr = min(tt * kBT + st_row[i], n_tok - 1) - tt * kBT;
+    offx[i] = uint32_t(tr) * uint32_t(row_stride) + st_chunk_off[i];
   }
-  auto set_w_offsets = [&](int vt) {
-#pragma unroll
-    for (int i = 0; i < G::kInstPerOperand; ++i) {
-      const int row = G::kRowsPerInst * (4 * i + wave) + lane / G::kChunks;
-      const int chunk = G::swz(row, lane % G::kChunks);
-      const int vr = min(vt * kBV + row, V - 1) - vt * kBV;
-      offw[i] = uint32_t(vr) * uint32_t(row_stride) + uint32_t(chunk * 16);
-    }
-  };
-  auto issue_stage = [&](int vt, int ks, int slot) {
-    char* base = lds + slot * G::kStageBytes;
+
+  // ---- prefetch: the loads of step pf_step = (pf_tile, pf_ks).  Steps past the
+  // end re-load the last stage into the slot being freed (never read), so every
+  // step issues exactly kLoadsPerStage loads per wave and the waits below are
+  // the same on every step; the loop body stays one basic block.
+  int pf_tile = 0, pf_ks = 0, pf_step = 0;
+  auto issue_next = [&]() {
+    const bool live = pf_tile < n_my_tiles;
+    const int vt = vs + (live ? pf_tile : n_my_tiles - 1) * n_vsplit;
+    const int ks = live ? pf_ks : nk - 1;
+    char* base = lds + (pf_step % S) * G::kStageBytes;
     const char* wk = reinterpret_cast<const char*>(W) + size_t(vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
     const char* xk = xt + size_t(ks) * G::kRowBytes;
 #pragma unroll
     for (int i = 0; i < G::kInstPerOperand; ++i) {
-      char* dst = base + G::kRowsPerInst * (4 * i + wave) * G::kRowBytes;
-      lds_dma16(wk + offw[i], dst);
+      const int vr = min(vt * kBV + st_row[i], V - 1) - vt * kBV;
+      char* dst = base + G::kRowsPerInst * (NW * i + wave) * G::kRowBytes;
+      lds_dma16(wk + (uint32_t(vr) * uint32_t(row_stride) + st_chunk_off[i]), dst);
       lds_dma16(xk + offx[i], dst + kBV * G::kRowBytes);
     }
+    ++pf_step;
+    const bool wrap = pf_ks + 1 == nk;
+    pf_ks = wrap ? 0 : pf_ks + 1;
+    pf_tile = wrap ? pf_tile + 1 : pf_tile;
   };
 
-  // ---- prefetch state: the step (tile index, depth stage) whose loads are issued next
-  int pf_tile = 0, pf_ks = 0, pf_step = 0;
-  set_w_offsets(vs);
-  auto issue_next = [&]() {
-    if (pf_step < n_steps) {
-      issue_stage(vs + pf_tile * n_vsplit, pf_ks, pf_step % S);
-      ++pf_step;
-      if (++pf_ks == nk) {
-        pf_ks = 0;
-        ++pf_tile;
-        if (pf_tile < n_my_tiles) set_w_offsets(vs + pf_tile * n_vsplit);
-      }
-    }
-  };
-#pragma unroll
-  for (int p = 0; p < S - 1; ++p) issue_next();
-
-  // ---- per-lane entropy state for the 4 token columns this lane owns
-  Ent2 st[4];
-#pragma unroll
-  for (int cb = 0; cb < 4; ++cb) st[cb] = Ent2{-INFINITY, 0.f, 0.f};
-
+  // ---- fragment reads: lane (row r = lane % 32, half h = lane / 32) reads 8 bf16 at
+  // k offset 16 kk + 8 h of row r of each 32-row block.
   const int frag_row = lane & 31;
   const int frag_half = lane >> 5;
-  int ra[4], rb[4];
+  uint32_t fa_off[2][4], fb_off[2][JT];  // byte offsets inside a stage, per k step
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = wv * 128 + i * 32 + frag_row;
-    rb[i] = wt * 128 + i * 32 + frag_row;
+  for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ra = wv * 128 + i * 32 + frag_row;
+      fa_off[kk][i] = ra * G::kRowBytes + G::swz(ra, kk * 2 + frag_half) * 16;
+    }
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+      const int rb = wt * G::TW + j * 32 + frag_row;
+      fb_off[kk][j] = kBV * G::kRowBytes + rb * G::kRowBytes + G::swz(rb, kk * 2 + frag_half) * 16;
+    }
   }
+  auto read_frags = [&](Frags<JT>& f, int slot, int kk) {
+    const char* base = lds + slot * G::kStageBytes;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(base + fa_off[kk][i]);
+#pragma unroll
+    for (int j = 0; j < JT; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(base + fb_off[kk][j]);
+  };
+  constexpr int kReads = 4 + JT;       // LDS reads per k step
+  constexpr int kMfma = 4 * JT;        // MFMAs per k step
+
+  // ---- per-lane entropy state for the JT token columns this lane owns
+  Ent2 st[JT];
+#pragma unroll
+  for (int cb = 0; cb < JT; ++cb) st[cb] = Ent2{-INFINITY, 0.f, 0.f};
+
+  // ---- prologue: stages 0 .. S-2 in flight; wait for stage 0, read its first fragments
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p) issue_next();
+  wait_vm<(S - 2) * G::kLoadsPerStage>();
+  lds_barrier();
+  Frags<JT> f0, f1;
+  read_frags(f0, 0, 0);
 
   for (int tile = 0; tile < n_my_tiles; ++tile) {
-    f32x16_t acc[4][4];
+    f32x16_t acc[4][JT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < JT; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     for (int ks = 0; ks < nk; ++ks) {
-    const int step = tile * nk + ks;
-    // stage `step` must have landed (own loads), then be visible from every wave;
-    // the barrier also retires all reads of the slot the next prefetch overwrites.
-    if (n_steps - 1 - step >= S - 2) {
-      wait_vm<(S - 2) * kLoadsPerStage>();
-    } else {
-      wait_vm<0>();
-    }
-    __syncthreads();
-    issue_next();
-
-    const char* sa = lds + (step % S) * G::kStageBytes;
-    const char* sb = sa + kBV * G::kRowBytes;
-    bf16x8_t fa[2][4], fb[2][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[0][i] = *reinterpret_cast<const bf16x8_t*>(sa + ra[i] * G::kRowBytes + G::swz(ra[i], frag_half) * 16);
-      fb[0][i] = *reinterpret_cast<const bf16x8_t*>(sb + rb[i] * G::kRowBytes + G::swz(rb[i], frag_half) * 16);
-    }
-#pragma unroll
-    for (int kk = 0; kk < kKK; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < kKK) {
-        const int chunk = (kk + 1) * 2 + frag_half;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          fa[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t*>(sa + ra[i] * G::kRowBytes + G::swz(ra[i], chunk) * 16);
-          fb[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t*>(sb + rb[i] * G::kRowBytes + G::swz(rb[i], chunk) * 16);
-        }
-      }
+      const int step = tile * nk + ks;
+      const int slot = step % S;
+      // Phase A: k step 0 of this stage on f0 while the k step 1 fragments load.
+      read_frags(f1, slot, 1);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
-    }
-
-    }  // ks
-
-    {
-      // ---- fold the finished tile into the running states, one 32 x 32 block at a
-      // time.  acc[i][j][r] is the logit of vocabulary row
-      // vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4 for token
-      // tt*256 + wt*128 + j*32 + frag_row.
-      const int vt = vs + tile * n_vsplit;
-      const int vbase = vt * kBV + wv * 128 + 4 * frag_half;
-      const bool ragged = (vt + 1) * kBV > V;
+        for (int j = 0; j < JT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[i], f0.b[j], acc[i][j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        Ent2 e = st[j];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float z[16];
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            z[r] = acc[i][j][r];
-            if (ragged && vbase + i * 32 + 8 * (r >> 2) + (r & 3) >= V) z[r] = -INFINITY;
-          }
-          float mx = z[0];
-#pragma unroll
-          for (int r = 1; r < 16; ++r) mx = fmaxf(mx, z[r]);
-          const float mnew = fmaxf(e.m, mx * kLog2e);
-          const float dl = fmaxf(e.m - mnew, kExp2Floor);
-          const float f = fast_exp2(dl);
-          float s = f * e.s;
-          float t = f * (e.t + e.s * dl);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float dd = fmaxf(fmaf(z[r], kLog2e, -mnew), kExp2Floor);
-            const float p = fast_exp2(dd);
-            s += p;
-            t = fmaf(p, dd, t);
-          }
-          e = Ent2{mnew, s, t};
-        }
-        st[j] = e;
+      for (int q = 0; q < kReads; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
       }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+
+      // Stage step+1 must be in LDS before anyone reads it; after this barrier
+      // every wave has also finished with slot (step-1) % S, which the next
+      // prefetch overwrites.  Issued after stage step+1: S-3 stages.
+      // Every read of slot (step-1) % S fed an MFMA of step step-1 already.
+      wait_vm<(S - 3) * G::kLoadsPerStage>();
+      ring_barrier();
+
+      // Phase B: k step 1 on f1 while the next stage's first fragments load and
+      // the prefetch of stage step+S-1 is issued.
+      read_frags(f0, (step + 1) % S, 0);  // past the last step: read and never used
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < JT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[i], f1.b[j], acc[i][j], 0, 0, 0);
+      issue_next();
+#pragma unroll
+      for (int q = 0; q < kReads; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
     }
-  }  // tile
+
+    // ---- fold the finished tile into the running states, one 32 x 32 block at a
+    // time.  acc[i][j][r] is the logit of vocabulary row
+    // vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4 for token
+    // tt*256 + wt*TW + j*32 + frag_row.
+    const int vt = vs + tile * n_vsplit;
+    const int vbase = vt * kBV + wv * 128 + 4 * frag_half;
+    const bool ragged = (vt + 1) * kBV > V;
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+      Ent2 e = st[j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float z[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          z[r] = acc[i][j][r];
+          if (ragged && vbase + i * 32 + 8 * (r >> 2) + (r & 3) >= V) z[r] = -INFINITY;
+        }
+        float mx = z[0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, z[r]);
+        const float mnew = fmaxf(e.m, mx * kLog2e);
+        const float dl = fmaxf(e.m - mnew, kExp2Floor);
+        const float f = fast_exp2(dl);
+        float s = f * e.s;
+        float t = f * (e.t + e.s * dl);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float dd = fmaxf(fmaf(z[r], kLog2e, -mnew), kExp2Floor);
+          const float p = fast_exp2(dd);
+          s += p;
+          t = fmaf(p, dd, t);
+        }
+        e = Ent2{mnew, s, t};
+        __builtin_amdgcn_sched_barrier(0);  // fold block by block: bounds live accumulator copies
+      }
+      st[j] = e;
+    }
+  }
 
   // ---- lanes l and l+32 hold the same tokens: merge them
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < JT; ++j) {
     Ent2 o;
     o.m = __shfl_xor(st[j].m, 32, 64);
     o.s = __shfl_xor(st[j].s, 32, 64);
@@ -256,12 +283,12 @@ __global__ __launch_bounds__(kThreads, 1) void entropy_gemm_kernel(
     st[j] = ent2_merge(st[j], o);
   }
   // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS
-  __syncthreads();  // every wave is done reading the ring
-  float* xbuf = reinterpret_cast<float*>(lds);  // [2 (wt)][128 tokens][3]
+  __syncthreads();  // every wave is done with the ring (no loads remain in flight)
+  float* xbuf = reinterpret_cast<float*>(lds);  // [256 tokens][3]
   if (wv == 1 && frag_half == 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float* p = xbuf + (wt * 128 + j * 32 + frag_row) * 3;
+    for (int j = 0; j < JT; ++j) {
+      float* p = xbuf + (wt * G::TW + j * 32 + frag_row) * 3;
       p[0] = st[j].m;
       p[1] = st[j].s;
       p[2] = st[j].t;
@@ -270,8 +297,8 @@ __global__ __launch_bounds__(kThreads, 1) void entropy_gemm_kernel(
   __syncthreads();
   if (wv == 0 && frag_half == 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tl = wt * 128 + j * 32 + frag_row;
+    for (int j = 0; j < JT; ++j) {
+      const int tl = wt * G::TW + j * 32 + frag_row;
       const float* p = xbuf + tl * 3;
       Ent2 r = ent2_merge(st[j], Ent2{p[0], p[1], p[2]});
       const int tok = tt * kBT + tl;
@@ -353,7 +380,7 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pt = c.take<float>(size_t(n_vsplit) * n);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  entropy_gemm_kernel<kBK, kStages><<<dim3(n_vsplit * n_tt), dim3(kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+  entropy_gemm_kernel<kStages, kWaves><<<dim3(n_vsplit * n_tt), dim3(Geom<kWaves>::kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
   ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");

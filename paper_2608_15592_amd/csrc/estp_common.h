@@ -30,9 +30,37 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* dst_wave_base) 
 #endif
 }
 
-// Wait until every outstanding vector-memory load of this wave has landed,
-// including global -> LDS transfers (s_waitcnt vmcnt(0); other counters untouched).
-__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N): wait until at most N of this wave's vector-memory
+// operations are outstanding (they retire in issue order), including global ->
+// LDS transfers; other counters untouched.  gfx9 encoding: vmcnt[3:0] |
+// expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at bits [15:14].
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Workgroup barrier that leaves outstanding global loads in flight (unlike
+// __syncthreads, whose fence drains them): waits only for this wave's LDS
+// operations, then s_barrier.  The signal fences keep the compiler from moving
+// memory accesses across it.  Visibility of global -> LDS transfers is the
+// caller's job (wait_vm before the barrier).
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Barrier for a ring whose slots are only ever written by global -> LDS
+// transfers: no LDS wait at all.  Safe when every LDS read of the slot that is
+// refilled after this barrier has already been consumed (its data used) by the
+// reading wave before the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
