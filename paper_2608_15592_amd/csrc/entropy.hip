@@ -70,6 +70,19 @@ struct Frags {
   bf16x8_t a[4], b[JT];
 };
 
+// Scheduling hint for one k step: its LDS fragment reads go out two per MFMA
+// at the front, so each has at least the remaining MFMAs of the step to land.
+template <int kReads, int kMfma>
+__device__ __forceinline__ void schedule_reads_front() {
+  constexpr int kGroups = (kReads + 1) / 2;
+#pragma unroll
+  for (int q = 0; q < kGroups; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kGroups, 0);
+}
+
 template <int S, int NW>
 __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
@@ -202,12 +215,7 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
 #pragma unroll
         for (int j = 0; j < JT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[i], f0.b[j], acc[i][j], 0, 0, 0);
-#pragma unroll
-      for (int q = 0; q < kReads; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+      schedule_reads_front<kReads, kMfma>();
 
       // Stage step+1 must be in LDS before anyone reads it; after this barrier
       // every wave has also finished with slot (step-1) % S, which the next
@@ -225,12 +233,7 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
         for (int j = 0; j < JT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[i], f1.b[j], acc[i][j], 0, 0, 0);
       issue_next();
-#pragma unroll
-      for (int q = 0; q < kReads; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+      schedule_reads_front<kReads, kMfma>();
     }
 
     // ---- fold the finished tile into the running states, one 32 x 32 block at a

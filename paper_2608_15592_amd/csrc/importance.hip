@@ -3,34 +3,61 @@
 // with A the causal softmax of scale * q_i . k_j inside each prompt, without
 // ever forming the N x N attention.
 //
-// Pass 1 (attn_lse_kernel) computes, for every (layer, query head, query row),
-// the base-2 log-sum-exp of its causal score row.  Scores are formed on the
-// matrix cores as S^T = K Q^T (keys on the MFMA "M" side, queries on "N"), so
-// a lane owns one query column and 16 key rows of each 32 x 32 block and the
-// row reduction over keys is a per-lane online max / sum.
+// Pass 1 (attn_lse_kernel): one workgroup per (layer, query head, prompt,
+// 256-query block); each of its 4 waves keeps 64 queries as matrix-core B
+// fragments in registers and streams the prompt's 64-key blocks through a
+// double-buffered LDS tile (global -> LDS transfers, chunk-swizzled).  Scores
+// are formed as S^T = K Q^T (keys on the MFMA "M" side), so a lane owns one
+// query column and 32 key rows of each block: the online max / sum over keys
+// is per lane.  Output: lse2 = log2 sum_j 2^(c s_ij), c = scale * log2 e.
 //
-// Pass 2 (attn_colsum_kernel) walks, for one 64-key block and one KV head,
-// every later query block of every query head that shares that KV head
-// (grouped-query reuse: the key fragments are loaded once and stay in
-// registers), re-forms S = Q K^T (queries on "M", keys on "N"), and adds
-// 2^(s2 - lse2) into per-lane column sums: a lane owns one key column and 16
-// query rows, so the sum over queries is again per lane until a final
-// two-step reduction (lane pair, then the four waves through LDS).  Partial
-// column masses are written per (layer, KV head) and reduced in a fixed
-// order by attn_reduce_kernel, which divides by N * Hq.  No atomics: results
-// are bitwise reproducible.
+// Pass 2 (attn_colsum_kernel): one workgroup per (layer, KV head, prompt,
+// 256-key block); each wave keeps 64 keys as B fragments in registers and
+// streams, through LDS, every later 32-query block of every query head that
+// shares the KV head (grouped-query reuse: the keys are read once).  Scores
+// are formed as S = Q K^T, so a lane owns one key column and 16 query rows of
+// each 32 x 32 block; 2^(c s - lse2) is summed per lane into column sums.
+// Partial column masses per (layer, KV head) are reduced in a fixed order by
+// attn_reduce_kernel, which divides by N * Hq.  No atomics: results are
+// bitwise reproducible.
 #include "estp_common.h"
 
 namespace estp {
 namespace detail {
 
 constexpr int kThreads = 256;
-constexpr int kQBlock = 64;  // query rows per pass-1 workgroup
-constexpr int kKBlock = 64;  // key columns per pass-2 workgroup
+constexpr int kQPerWave = 64;  // queries per wave in pass 1
+constexpr int kQBlock = 4 * kQPerWave;
+constexpr int kKPerWave = 64;  // keys per wave in pass 2
+constexpr int kKBlock = 4 * kKPerWave;
+constexpr int kKTile = 64;     // keys per streamed tile in pass 1
+constexpr int kQTile = 32;     // queries per streamed tile in pass 2
 
-// Fragment of 8 consecutive bf16 of one row: row-major [*, row_stride] halves.
-__device__ __forceinline__ bf16x8_t load_frag(const uint16_t* p) {
-  return *reinterpret_cast<const bf16x8_t*>(p);
+// Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
+// consecutive rows read at one logical chunk hit 16 distinct bank groups.
+template <int DH>
+struct RowTile {
+  static constexpr int kRowBytes = DH * 2;
+  static constexpr int kChunks = kRowBytes / 16;
+  static constexpr int kRowsPerInst = 64 / kChunks;  // rows one wave-wide 16-byte transfer fills
+  static constexpr int kRowsPerWindow = kRowBytes >= 256 ? 1 : 256 / kRowBytes;
+  __device__ static __forceinline__ int swz(int row, int chunk) {
+    return chunk ^ ((row / kRowsPerWindow) & (kChunks - 1));
+  }
+  // byte offset of the fragment (row, logical chunk)
+  __device__ static __forceinline__ int off(int row, int chunk) { return row * kRowBytes + swz(row, chunk) * 16; }
+};
+
+// Wave-cooperative staging of `rows` rows into LDS at `dst`; tile row r comes
+// from `src_row(r)`.  Waves take groups of kRowsPerInst rows round-robin.
+template <int DH, typename RowPtr>
+__device__ __forceinline__ void stage_rows(char* dst, int rows, int wave, int nwaves, int lane, RowPtr src_row) {
+  using T = RowTile<DH>;
+  for (int r0 = wave * T::kRowsPerInst; r0 < rows; r0 += nwaves * T::kRowsPerInst) {
+    const int r = r0 + lane / T::kChunks;
+    const int chunk = T::swz(r, lane % T::kChunks);
+    lds_dma16(reinterpret_cast<const char*>(src_row(r)) + chunk * 16, dst + r0 * T::kRowBytes);
+  }
 }
 
 // ---------------------------------------------------------------- pass 1
@@ -41,71 +68,111 @@ __global__ __launch_bounds__(kThreads) void attn_lse_kernel(const uint16_t* __re
                                                             int L, int Hq, int Hkv, int nqb_max, float c2,
                                                             float* __restrict__ lse2) {
   constexpr int KS = DH / 16;
-  const int G = Hq / Hkv;
-  // block -> (query block, prompt, layer * Hkv + kv head); largest query blocks first
+  using T = RowTile<DH>;
+  constexpr int kTileBytes = kKTile * T::kRowBytes;
+  __shared__ __attribute__((aligned(16))) char ktile[2][kTileBytes];
+
+  // block -> (query block, prompt, layer * Hq + head); largest query blocks first
   int idx = blockIdx.x;
-  const int lg = idx % (L * Hkv);
-  idx /= L * Hkv;
+  const int lh = idx % (L * Hq);
+  idx /= L * Hq;
   const int b = idx % B;
   const int qblk = nqb_max - 1 - idx / B;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   if (qblk * kQBlock >= N) return;
-  const int l = lg / Hkv, g = lg % Hkv;
+  const int l = lh / Hq, h = lh % Hq;
+  const int g = h / (Hq / Hkv);
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 31;   // query column of this lane in a 32 x 32 block
-  const int half = lane >> 5;  // which 8-wide k half of the fragment / which row quad of the output
+  const int half = lane >> 5;  // 8-wide k half of the fragment / row quad of the output
   const size_t qrow = size_t(Hq) * DH, krow = size_t(Hkv) * DH;
-  const uint16_t* Kl = K + size_t(l) * n_tok * krow + size_t(base) * krow + size_t(g) * DH;
+  const uint16_t* Qh = Q + size_t(l) * n_tok * qrow + size_t(base) * qrow + size_t(h) * DH;
+  const uint16_t* Kg = K + size_t(l) * n_tok * krow + size_t(base) * krow + size_t(g) * DH;
 
-  // units: (head in group, 32-row half of the query block), dealt to waves round-robin
-  for (int u = wave; u < 2 * G; u += 4) {
-    const int h = g * G + (u >> 1);
-    const int q0 = qblk * kQBlock + (u & 1) * 32;
-    if (q0 >= N) continue;
-    const int qi = min(q0 + col, N - 1);
-    const uint16_t* qp = Q + size_t(l) * n_tok * qrow + size_t(base + qi) * qrow + size_t(h) * DH + half * 8;
-    bf16x8_t bq[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) bq[ks] = load_frag(qp + ks * 16);
+  const int q0 = qblk * kQBlock + wave * kQPerWave;  // this wave's first query
+  const int q_hi = min(N, qblk * kQBlock + kQBlock);  // end of the block's queries
+  const int n_kt = (q_hi - 1) / kKTile + 1;           // key tiles the block needs
 
-    float m = -INFINITY, s = 0.f;
-    const int q_last = q0 + col;  // this lane's query (may be >= N in a ragged tail)
-    for (int kb = 0; kb <= q0 / 32; ++kb) {
-      const int kj = min(kb * 32 + col, N - 1);
-      const uint16_t* kp = Kl + size_t(kj) * krow + half * 8;
-      f32x16_t acc;
+  // queries as B fragments: column cb*32 + col, k = 16 ks + 8 half
+  bf16x8_t bq[2][KS];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int cb = 0; cb < 2; ++cb) {
+    const int qi = min(q0 + cb * 32 + col, N - 1);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(load_frag(kp + ks * 16), bq[ks], acc, 0, 0, 0);
-      // acc[r]: key kb*32 + 8*(r/4) + 4*half + r%4, query q0 + col
-      float z[16];
-      float mx = -INFINITY;
-      const bool diag = (kb == q0 / 32);
+    for (int ks = 0; ks < KS; ++ks)
+      bq[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Qh + size_t(qi) * qrow + ks * 16 + half * 8);
+  }
+  float m[2] = {-INFINITY, -INFINITY}, s[2] = {0.f, 0.f};
+
+  auto stage = [&](int kt, int buf) {
+    stage_rows<DH>(ktile[buf], kKTile, wave, 4, lane,
+                   [&](int r) { return Kg + size_t(min(kt * kKTile + r, N - 1)) * krow; });
+  };
+  stage(0, 0);
+  for (int kt = 0; kt < n_kt; ++kt) {
+    wait_vm<0>();
+    lds_barrier();  // tile kt visible; every wave is done with buffer (kt + 1) & 1
+    if (kt + 1 < n_kt) stage(kt + 1, (kt + 1) & 1);
+    const int k0 = kt * kKTile;
+    if (k0 > q0 + kQPerWave - 1 || q0 >= N) continue;  // whole tile after this wave's queries
+    const char* kb = ktile[kt & 1];
+    f32x16_t acc[2][2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        z[r] = (!diag || j <= q_last) ? acc[r] * c2 : -INFINITY;
-        mx = fmaxf(mx, z[r]);
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + T::off(rb * 32 + col, ks * 2 + half));
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[cb][ks], acc[rb][cb], 0, 0, 0);
       }
-      const float mnew = fmaxf(m, mx);
-      const float f = fast_exp2(fmaxf(m - mnew, kExp2Floor));
-      s *= f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s += fast_exp2(fmaxf(z[r] - mnew, kExp2Floor));
-      m = mnew;
     }
-    // lanes col and col + 32 hold the two row-quads of the same query column
-    const float mo = __shfl_xor(m, 32, 64);
-    const float so = __shfl_xor(s, 32, 64);
-    const float M = fmaxf(m, mo);
-    const float tot = s * fast_exp2(fmaxf(m - M, kExp2Floor)) + so * fast_exp2(fmaxf(mo - M, kExp2Floor));
-    if (half == 0 && q0 + col < N)
-      lse2[(size_t(l) * Hq + h) * n_tok + base + q0 + col] = M + fast_log2(tot);
+    // acc[rb][cb][r]: key k0 + rb*32 + 8*(r/4) + 4*half + r%4, query q0 + cb*32 + col
+    const bool diag = k0 + kKTile - 1 > q0;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      const int qi = q0 + cb * 32 + col;
+      if (diag) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (k0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) > qi) acc[rb][cb][r] = -INFINITY;
+      }
+      float mx = acc[0][cb][0];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
+      const float mnew = fmaxf(m[cb], mx * c2);
+      float sum = s[cb] * fast_exp2(fmaxf(m[cb] - mnew, kExp2Floor));
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[rb][cb][r], c2, -mnew));
+      // nothing seen yet in this lane (all keys masked): fmaf(-inf, c2, inf) is NaN, keep the empty state
+      s[cb] = (mnew == -INFINITY) ? 0.f : sum;
+      m[cb] = mnew;
+    }
+  }
+  // lanes col and col + 32 hold the two row quads of the same query column
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    const float mo = __shfl_xor(m[cb], 32, 64);
+    const float so = __shfl_xor(s[cb], 32, 64);
+    const float M = fmaxf(m[cb], mo);
+    const float tot = s[cb] * fast_exp2(fmaxf(m[cb] - M, kExp2Floor)) + so * fast_exp2(fmaxf(mo - M, kExp2Floor));
+    const int qi = q0 + cb * 32 + col;
+    if (half == 0 && qi < N) lse2[(size_t(l) * Hq + h) * n_tok + base + qi] = M + fast_log2(tot);
   }
 }
 
@@ -118,7 +185,11 @@ __global__ __launch_bounds__(kThreads) void attn_colsum_kernel(const uint16_t* _
                                                                const float* __restrict__ lse2,
                                                                float* __restrict__ part) {
   constexpr int KS = DH / 16;
-  __shared__ float red[4][kKBlock];
+  using T = RowTile<DH>;
+  constexpr int kTileBytes = kQTile * T::kRowBytes;
+  __shared__ __attribute__((aligned(16))) char qtile[2][kTileBytes];
+  __shared__ __attribute__((aligned(16))) float ltile[2][kQTile];
+
   const int G = Hq / Hkv;
   // block -> (key block, prompt, layer * Hkv + kv head); key block 0 (the most work) first
   int idx = blockIdx.x;
@@ -132,73 +203,107 @@ __global__ __launch_bounds__(kThreads) void attn_colsum_kernel(const uint16_t* _
   const int l = lg / Hkv, g = lg % Hkv;
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 31;   // key column of this lane in a 32 x 32 block
   const int half = lane >> 5;
   const size_t qrow = size_t(Hq) * DH, krow = size_t(Hkv) * DH;
-  const uint16_t* Kl = K + size_t(l) * n_tok * krow + size_t(base) * krow + size_t(g) * DH;
+  const uint16_t* Ql = Q + size_t(l) * n_tok * qrow + size_t(base) * qrow;
+  const uint16_t* Kg = K + size_t(l) * n_tok * krow + size_t(base) * krow + size_t(g) * DH;
+  const float* Ll = lse2 + size_t(l) * Hq * n_tok + base;
 
-  // key fragments of the two 32-key halves, resident for the whole walk
+  const int k0 = kblk * kKBlock + wave * kKPerWave;  // this wave's first key
+  // keys as B fragments, resident for the whole walk
   bf16x8_t bk[2][KS];
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    const int kj = min(kblk * kKBlock + cb * 32 + col, N - 1);
+    const int kj = min(k0 + cb * 32 + col, N - 1);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) bk[cb][ks] = load_frag(Kl + size_t(kj) * krow + half * 8 + ks * 16);
+    for (int ks = 0; ks < KS; ++ks)
+      bk[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Kg + size_t(kj) * krow + ks * 16 + half * 8);
   }
   float csum[2] = {0.f, 0.f};
 
-  const int qb_first = kblk * (kKBlock / 32);
-  const int qb_end = (N + 31) / 32;
-  const int n_pairs = (qb_end - qb_first) * G;
-  for (int p = wave; p < n_pairs; p += 4) {
-    const int h = g * G + p % G;
-    const int qb = qb_first + p / G;
-    const int qi = min(qb * 32 + col, N - 1);
-    const uint16_t* qp = Q + size_t(l) * n_tok * qrow + size_t(base + qi) * qrow + size_t(h) * DH + half * 8;
-    bf16x8_t aq[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) aq[ks] = load_frag(qp + ks * 16);
-    // lse of the 16 query rows this lane sees: rows qb*32 + 8*(r/4) + 4*half + r%4
-    const float* lp = lse2 + (size_t(l) * Hq + h) * n_tok + base;
-    float lr[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = qb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-      lr[r] = i < N ? lp[i] : INFINITY;  // rows past the prompt contribute 2^-inf = 0
+  // tiles: (query block qb, head) for qb from the block's first key on; head fastest
+  const int qb_first = kblk * (kKBlock / kQTile);
+  const int n_qb = (N + kQTile - 1) / kQTile - qb_first;
+  const int n_tiles = n_qb * G;
+  auto stage = [&](int t, int buf) {
+    const int hh = g * G + t % G;
+    const int qb = qb_first + t / G;
+    stage_rows<DH>(qtile[buf], kQTile, wave, 4, lane,
+                   [&](int r) { return Ql + size_t(min(qb * kQTile + r, N - 1)) * qrow + size_t(hh) * DH; });
+  };
+  auto lse_load = [&](int t) {  // lanes 0..31 of wave 0 fetch the tile's 32 row LSEs
+    const int hh = g * G + t % G;
+    const int i = (qb_first + t / G) * kQTile + lane;
+    return (lane < kQTile && i < N) ? Ll[size_t(hh) * n_tok + i] : INFINITY;  // rows past N weigh 0
+  };
+
+  stage(0, 0);
+  float lv = (wave == 0) ? lse_load(0) : 0.f;
+  if (wave == 0 && lane < kQTile) ltile[0][lane] = lv;
+  for (int t = 0; t < n_tiles; ++t) {
+    wait_vm<0>();
+    lds_barrier();  // tile t (queries and LSEs) visible; every wave is done with buffer (t + 1) & 1
+    const bool more = t + 1 < n_tiles;
+    if (more) {
+      stage(t + 1, (t + 1) & 1);
+      if (wave == 0) lv = lse_load(t + 1);
     }
+    const int qb = qb_first + t / G;
+    const int i0 = qb * kQTile;
+    if (i0 + kQTile - 1 >= k0 && k0 < N) {  // some query of the tile sees some key of this wave
+      const char* qt = qtile[t & 1];
+      f32x16_t acc[2];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      const int j = kblk * kKBlock + cb * 32 + col;  // this lane's key
-      if (qb * 32 + 31 < kblk * kKBlock + cb * 32) continue;  // whole block above the diagonal
-      f32x16_t acc;
+      for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[ks], bk[cb][ks], acc, 0, 0, 0);
-      float cs = 0.f;
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(col, ks * 2 + half));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = qb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float pr = fast_exp2(fmaxf(fmaf(acc[r], c2, -lr[r]), kExp2Floor));
-        cs += (j <= i) ? pr : 0.f;
+        for (int cb = 0; cb < 2; ++cb)
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[cb], 0, 0, 0);
       }
-      csum[cb] += cs;
-    }
-  }
-  // reduce: lane pair (the two row quads), then the four waves in fixed order
+      // acc[cb][r]: query i0 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
+      float lr[16];
+      const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) csum[cb] += __shfl_xor(csum[cb], 32, 64);
-  if (half == 0) {
-    red[wave][col] = csum[0];
-    red[wave][32 + col] = csum[1];
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 v = lp[2 * q4 + half];  // rows 8 q4 + 4 half .. + 3
+        lr[4 * q4] = v.x;
+        lr[4 * q4 + 1] = v.y;
+        lr[4 * q4 + 2] = v.z;
+        lr[4 * q4 + 3] = v.w;
+      }
+      const bool diag = i0 < k0 + kKPerWave - 1;
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        const int j = k0 + cb * 32 + col;
+        float cs = 0.f;
+        if (diag) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
+            const float p = fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
+            cs += (j <= i) ? p : 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) cs += fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
+        }
+        csum[cb] += cs;
+      }
+    }
+    if (more && wave == 0 && lane < kQTile) ltile[(t + 1) & 1][lane] = lv;
   }
-  __syncthreads();
-  if (threadIdx.x < kKBlock) {
-    const int t = threadIdx.x;
-    const float v = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
-    const int j = kblk * kKBlock + t;
-    if (j < N) part[(size_t(l) * Hkv + g) * n_tok + base + j] = v;
+  // the two row quads (lane, lane + 32) of each key column
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    csum[cb] += __shfl_xor(csum[cb], 32, 64);
+    const int j = k0 + cb * 32 + col;
+    if (half == 0 && j < N) part[(size_t(l) * Hkv + g) * n_tok + base + j] = csum[cb];
   }
 }
 
@@ -221,8 +326,10 @@ void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
   const int nkb = (max_seqlen + kKBlock - 1) / kKBlock;
-  attn_lse_kernel<DH><<<dim3(size_t(nqb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2, lse2);
-  attn_colsum_kernel<DH><<<dim3(size_t(nkb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2, lse2, part);
+  attn_lse_kernel<DH><<<dim3(size_t(nqb) * B * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
+                                                                                 nqb, c2, lse2);
+  attn_colsum_kernel<DH><<<dim3(size_t(nkb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
+                                                                                    c2, lse2, part);
   attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L * Hkv, Hq, S);
 }
 
