@@ -1,6 +1,6 @@
 // Length head (Section 4.3) and shortest-job-first order (Section 5.4).
 //
-//   a = act(W1 h + b1)            mlp_hidden_kernel: fp32 tiled GEMM [B, d] x [hidden, d]^T
+//   a = act(W1 h + b1)            mlp_partial_kernel (split-K fp32 tiles) + mlp_finish_kernel
 //   o = W2 a + b2                 head_out_kernel: one workgroup per prompt
 //   K == 1: yhat = o_0;  K > 1: p = softmax(o), yhat = sum_k p_k c_k (Eq. 7), bin = argmax p
 //   order: stable ascending argsort of yhat (rank counting, exact and deterministic)
@@ -9,9 +9,10 @@
 namespace estp {
 namespace detail {
 
-constexpr int kTB = 64;   // prompts per tile
-constexpr int kTH = 64;   // hidden units per tile
-constexpr int kTK = 16;   // reduction depth per LDS stage
+constexpr int kTB = 32;     // prompts per tile
+constexpr int kTH = 32;     // hidden units per tile
+constexpr int kTK = 32;     // reduction depth per LDS stage
+constexpr int kKChunk = 256;  // reduction range of one split-K workgroup
 
 __device__ __forceinline__ float act_fn(float x, int act) {
   if (act == ESTP_ACT_RELU) return fmaxf(x, 0.f);
@@ -20,47 +21,51 @@ __device__ __forceinline__ float act_fn(float x, int act) {
   return 0.5f * x * (1.f + tanhf(u));
 }
 
-// A[b, j] = act(sum_k P[b, k] W1[j, k] + b1[j]); 256 threads, each a 4 x 4 block of the 64 x 64 tile.
-__global__ __launch_bounds__(256) void mlp_hidden_kernel(const float* __restrict__ P, const float* __restrict__ W1,
-                                                         const float* __restrict__ b1, int B, int d, int Hd, int act,
-                                                         float* __restrict__ A) {
-  __shared__ float sp[kTK][kTB + 4];
-  __shared__ float sw[kTK][kTH + 4];
-  const int tb = blockIdx.y * kTB, th = blockIdx.x * kTH;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;  // 16 x 16 threads
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < d; k0 += kTK) {
-    // load a 64 x 16 slab of P and of W1 (transposed into [k][row])
+// Split-K partial of the first layer: part[z, b, j] = sum_{k in chunk z} P[b, k] W1[j, k].
+// 256 threads own a 32 x 32 (prompt x hidden) tile, 4 outputs each; the grid spans
+// hidden tiles x prompt tiles x reduction chunks so that W1 is streamed once by
+// hundreds of workgroups even for small batches.
+__global__ __launch_bounds__(256) void mlp_partial_kernel(const float* __restrict__ P, const float* __restrict__ W1,
+                                                          int B, int d, int Hd, float* __restrict__ part) {
+  __shared__ float sp[kTK][kTB + 1];
+  __shared__ float sw[kTK][kTH + 1];
+  const int th = blockIdx.x * kTH, tb = blockIdx.y * kTB, z = blockIdx.z;
+  const int k_lo = z * kKChunk, k_hi = min(d, k_lo + kKChunk);
+  const int tx = threadIdx.x & 31;         // hidden unit in the tile
+  const int ty = (threadIdx.x >> 5) * 4;   // first of 4 prompts
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = k_lo; k0 < k_hi; k0 += kTK) {
     for (int e = threadIdx.x; e < kTB * kTK; e += 256) {
-      const int r = e / kTK, k = e % kTK;
-      const int gb = tb + r, gk = k0 + k;
-      sp[k][r] = (gb < B && gk < d) ? P[size_t(gb) * d + gk] : 0.f;
-      const int gh = th + r;
-      sw[k][r] = (gh < Hd && gk < d) ? W1[size_t(gh) * d + gk] : 0.f;
+      const int r = e / kTK, k = e % kTK;  // consecutive threads read consecutive k of one row
+      const int gk = k0 + k;
+      sp[k][r] = (tb + r < B && gk < k_hi) ? P[size_t(tb + r) * d + gk] : 0.f;
+      sw[k][r] = (th + r < Hd && gk < k_hi) ? W1[size_t(th + r) * d + gk] : 0.f;
     }
     __syncthreads();
-#pragma unroll
+#pragma unroll 8
     for (int k = 0; k < kTK; ++k) {
-      float pa[4], wa[4];
+      const float w = sw[k][tx];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pa[i] = sp[k][ty * 4 + i];
-        wa[i] = sw[k][tx * 4 + i];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(pa[i], wa[j], acc[i][j]);
+      for (int i = 0; i < 4; ++i) acc[i] = fmaf(sp[k][ty + i], w, acc[i]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gb = tb + ty * 4 + i, gh = th + tx * 4 + j;
-      if (gb < B && gh < Hd) A[size_t(gb) * Hd + gh] = act_fn(acc[i][j] + (b1 ? b1[gh] : 0.f), act);
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int b = tb + ty + i, j = th + tx;
+    if (b < B && j < Hd) part[(size_t(z) * B + b) * Hd + j] = acc[i];
+  }
+}
+
+// A[b, j] = act(sum_z part[z, b, j] + b1[j]), chunks summed in order.
+__global__ __launch_bounds__(256) void mlp_finish_kernel(const float* __restrict__ part, const float* __restrict__ b1,
+                                                         int B, int Hd, int nz, int act, float* __restrict__ A) {
+  const size_t e = size_t(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= size_t(B) * Hd) return;
+  const int j = int(e % Hd);
+  float v = 0.f;
+  for (int z = 0; z < nz; ++z) v += part[size_t(z) * B * Hd + e];
+  A[e] = act_fn(v + (b1 ? b1[j] : 0.f), act);
 }
 
 // One workgroup (256 threads) per prompt: o = W2 a + b2, then y-hat and bin.
@@ -144,9 +149,10 @@ using namespace estp;
 using namespace estp::detail;
 
 extern "C" size_t estp_predict_workspace_size(int32_t B, int32_t d, int32_t hidden, int32_t K) {
-  (void)d;
-  if (B < 1 || hidden < 1 || K < 1) return 0;
+  if (B < 1 || hidden < 1 || K < 1 || d < 1) return 0;
+  const size_t nz = (size_t(d) + kKChunk - 1) / kKChunk;
   Carver c(nullptr);
+  c.take<float>(nz * B * hidden);     // split-K partials of the first layer
   c.take<float>(size_t(B) * hidden);  // hidden activations
   c.take<float>(size_t(B) * K);       // head outputs
   return c.bytes();
@@ -169,12 +175,17 @@ extern "C" int estp_predict(const float* pooled, int32_t B, int32_t d, const flo
                workspace_bytes, need);
   ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
                "estp_predict: workspace must be non-null and 256-byte aligned");
+  const int nz = (d + kKChunk - 1) / kKChunk;
   Carver c(workspace);
+  float* part = c.take<float>(size_t(nz) * B * hidden);
   float* A = c.take<float>(size_t(B) * hidden);
   float* o = c.take<float>(size_t(B) * K);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  mlp_hidden_kernel<<<dim3((hidden + kTH - 1) / kTH, (B + kTB - 1) / kTB), dim3(256), 0, s>>>(pooled, W1, b1, B, d, hidden, act, A);
-  ESTP_CHECK_LAUNCH("mlp_hidden_kernel");
+  mlp_partial_kernel<<<dim3((hidden + kTH - 1) / kTH, (B + kTB - 1) / kTB, nz), dim3(256), 0, s>>>(pooled, W1, B, d,
+                                                                                                 hidden, part);
+  ESTP_CHECK_LAUNCH("mlp_partial_kernel");
+  mlp_finish_kernel<<<dim3((size_t(B) * hidden + 255) / 256), dim3(256), 0, s>>>(part, b1, B, hidden, nz, act, A);
+  ESTP_CHECK_LAUNCH("mlp_finish_kernel");
   head_out_kernel<<<dim3(B), dim3(256), 0, s>>>(A, W2, b2, centres, hidden, K, o, yhat, K > 1 ? bin : nullptr);
   ESTP_CHECK_LAUNCH("head_out_kernel");
   if (order) {

@@ -183,9 +183,10 @@ def test_combine_pool_special_cases():
 
 # ------------------------------------------------------------------------------------------ length head
 
-@pytest.mark.parametrize("K,act", [(1, "relu"), (8, "relu"), (8, "gelu_tanh"), (1, "gelu_tanh")])
-def test_predict_parity(K, act):
-    B, d, Hdn = 37, 256, 96
+@pytest.mark.parametrize("K,act,B,d,Hdn", [(1, "relu", 37, 256, 96), (8, "relu", 37, 256, 96),
+                                          (8, "gelu_tanh", 37, 256, 96), (1, "gelu_tanh", 37, 256, 96),
+                                          (1, "relu", 70, 1000, 1024), (16, "relu", 3, 4096, 40)])
+def test_predict_parity(K, act, B, d, Hdn):
     g = np.random.default_rng(9)
     P = g.standard_normal((B, d)).astype(np.float32)
     W1 = (g.standard_normal((Hdn, d)) * 0.1).astype(np.float32)
