@@ -38,46 +38,52 @@ def to_dev(a, torch):
     return torch.from_numpy(a).cuda()
 
 
-def cpu_baseline(w, inp, lam1, lam2, alpha, norm, entropy_rows: int):
-    """The fp64 oracle on a bounded sample of the workload: prompt 0 whole for importance,
-    fusion, pooling and the head; its first `entropy_rows` tokens for the entropy."""
+def cpu_baseline(inp, lam1, lam2, alpha, norm, n_prompts: int):
+    """The fp64 oracle on a bounded sample of the same workload: its first `n_prompts`
+    whole prompts through the whole path (entropy, importance, fusion, pooling, head)."""
     import oracle
-    from synth import inputs as I
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
     except Exception:  # pragma: no cover
         blas_threads = 1
-    lengths = inp["lengths"]
-    N0 = int(lengths[0])
-    rows = np.arange(N0)
-    X0 = inp["X"][:N0]
+    cu = inp["cu_seqlens"].astype(np.int64)
+    n = int(cu[n_prompts])
+    cu_s = cu[: n_prompts + 1]
     t0 = time.perf_counter()
-    H0 = oracle.token_entropy(X0[:entropy_rows], inp["W"])
-    t_h = time.perf_counter() - t0
-    Q0 = inp["Q"][:, :N0]
-    K0 = inp["K"][:, :N0]
-    t0 = time.perf_counter()
-    S0 = oracle.attn_importance(Q0, K0, [0, N0])
-    t_s = time.perf_counter() - t0
-    Hfull = np.concatenate([H0, np.full(N0 - len(H0), float(np.mean(H0)))])
-    t0 = time.perf_counter()
-    e, _ = oracle.combine_weights(S0, Hfull, [0, N0], lam1, lam2, alpha, norm)
-    h = oracle.pool(X0, e, [0, N0])
-    oracle.predict(h, inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"])
-    t_p = time.perf_counter() - t0
-    per_tok = t_h / len(H0) + (t_s + t_p) / N0
-    del rows, I
+    out = oracle.run_path(inp["X"][:n], inp["W"], inp["Q"][:, :n], inp["K"][:, :n], cu_s, lam1, lam2, alpha, norm,
+                          head=(inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"]))
+    dt = time.perf_counter() - t0
+    del out
     return {
-        "value": 1.0 / per_tok,
+        "value": n / dt,
         "unit": "tokens/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"prompt 0 of the workload ({N0} tokens) for importance, fusion, pooling and head; "
-                   f"its first {len(H0)} tokens for the entropy; per-token costs summed "
-                   f"(entropy {t_h:.1f} s, importance {t_s:.1f} s, rest {t_p:.2f} s)"),
+        "sample": f"the first {n_prompts} whole prompts of the workload ({n} tokens), whole path, {dt:.1f} s",
         "host_cpus": len(os.sched_getaffinity(0)),
     }
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch of the entropy kernel from the committed rocprofv3 counter summary,
+    or None when that summary is for another workload or for a different kernel source."""
+    import hashlib
+    import re
+    if workload != "llama":
+        return None
+    path = os.path.join(ROOT, "profiles", "llama_path_hbm_counters.md")
+    try:
+        txt = open(path).read()
+    except OSError:
+        return None
+    m = re.search(r"entropy_gemm traffic_bytes=(\d+) source_sha256_16=([0-9a-f]+)", txt)
+    if not m:
+        return None
+    h = hashlib.sha256()
+    for f in ("paper_2608_15592_amd/csrc/entropy.hip", "paper_2608_15592_amd/csrc/estp_common.h"):
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return float(m.group(1)) if h.hexdigest()[:16] == m.group(2) else None
 
 
 def main() -> int:
@@ -92,7 +98,7 @@ def main() -> int:
     ap.add_argument("--alpha", type=float, default=1.0)
     ap.add_argument("--norm", default="none", choices=["none", "zscore"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--entropy-sample-rows", type=int, default=512)
+    ap.add_argument("--cpu-sample-prompts", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run 3 device-to-device copies of BYTES (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -209,7 +215,7 @@ def main() -> int:
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": ent_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": recorded_traffic(args.workload),
             "work_per_launch": f"2*n_tok*V*d = {ent_flop:.4g} FLOP",
         },
         "kernels_ms": {"token_entropy": ent_ms, "attn_importance": imp_ms, "combine_pool": pool_ms,
@@ -223,8 +229,8 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host sample ...")
-        result["cpu_baseline"] = cpu_baseline(w, inp, args.lambda1, args.lambda2, args.alpha, args.norm,
-                                              args.entropy_sample_rows)
+        result["cpu_baseline"] = cpu_baseline(inp, args.lambda1, args.lambda2, args.alpha, args.norm,
+                                              args.cpu_sample_prompts)
         log(f"oracle: {result['cpu_baseline']['value']:.1f} tokens/s")
     print(json.dumps(result), flush=True)
     return 0

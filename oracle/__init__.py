@@ -9,7 +9,8 @@ Every function takes bf16 bit patterns (uint16) or float arrays, widens them
 exactly to float64 and evaluates the paper's definitions:
 
 * ``token_entropy``      - Eq. 2 (Section 4.2)
-* ``attn_importance``    - Eq. 1 (Section 4.1)
+* ``attn_importance``    - Eq. 1 (Section 4.1); ``attn_importance_tail``
+  gives the same S_j for the last m keys of one prompt from its last m rows
 * ``combine_weights``    - Eq. 3 and Eq. 4 (Section 4.2)
 * ``pool``               - Eq. 5 (Section 4.2)
 * ``predict``            - the MLP length head with Eq. 7 (Section 4.3)
@@ -23,6 +24,7 @@ from .estp_oracle import (  # noqa: F401
     widen,
     token_entropy,
     attn_importance,
+    attn_importance_tail,
     combine_weights,
     pool,
     predict,

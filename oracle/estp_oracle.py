@@ -121,6 +121,36 @@ def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: 
     return S
 
 
+def attn_importance_tail(Q, K, N: int, m: int, scale: Optional[float] = None) -> np.ndarray:
+    """S_j of Eq. 1 for the last ``m`` keys j = N-m .. N-1 of ONE prompt of length N.
+
+    Only queries i >= j attend to key j under the causal mask, so these m
+    values need just the last m attention rows (each row still over all of
+    its i+1 keys).  ``Q`` [L, N, Hq, dh], ``K`` [L, N, Hkv, dh] hold that
+    prompt alone.  Returns [m], summed over layers like ``attn_importance``.
+    """
+    Qd = widen(Q)
+    Kd = widen(K)
+    if Qd.ndim == 3:
+        Qd, Kd = Qd[None], Kd[None]
+    L, n, Hq, dh = Qd.shape
+    if n != N or not 1 <= m <= N:
+        raise ValueError("Q, K must hold exactly the prompt and 1 <= m <= N")
+    G = Hq // Kd.shape[2]
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    i0 = N - m
+    S = np.zeros(m, dtype=np.float64)
+    for l in range(L):
+        colsum = np.zeros(m, dtype=np.float64)
+        for h in range(Hq):
+            s = scale * (Qd[l, i0:, h, :] @ Kd[l, :, h // G, :].T)   # rows i0..N-1, all keys
+            A = _causal_softmax_rows(s, i0)
+            colsum += A[:, i0:].sum(axis=0) / Hq
+        S += colsum / N
+    return S
+
+
 # ----------------------------------------------------------------------------- Eq. 3, 4
 
 def _zscore(v: np.ndarray, eps: float = 1e-6) -> np.ndarray:

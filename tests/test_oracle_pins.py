@@ -384,6 +384,20 @@ def test_importance_row_chunks_complete():
                                oracle.attn_importance(Q, K, [0, 23], row_chunk=4096), rtol=1e-14)
 
 
+def test_importance_tail_matches_whole_prompt():
+    # the last m keys only receive attention from the last m queries: the tail form is exact
+    N, L = 53, 2
+    Q = _rng(42).standard_normal((L, N, 4, 8)) * 1.5
+    K = _rng(43).standard_normal((L, N, 2, 8))
+    full = oracle.attn_importance(Q, K, [0, N])
+    for m in (1, 7, N):
+        np.testing.assert_allclose(oracle.attn_importance_tail(Q, K, N, m), full[N - m:], rtol=1e-13)
+    # and on the uniform case, the harmonic closed form
+    Q0 = np.zeros((1, N, 2, 4))
+    tail = oracle.attn_importance_tail(Q0, K[:1, :, :2, :4], N, 10)
+    np.testing.assert_allclose(tail, [(_harm(N) - _harm(j)) / N for j in range(N - 10, N)], rtol=1e-13)
+
+
 def test_widen_bf16_exact():
     bits = np.array([0x3F80, 0xBF80, 0x4049, 0x0001, 0x7F7F, 0x0000], dtype=np.uint16)
     got = oracle.widen(bits)
