@@ -29,7 +29,6 @@ namespace estp {
 namespace detail {
 
 constexpr int kBV = 256;       // vocabulary rows per tile
-constexpr int kBT = 256;       // tokens per tile
 constexpr int kMaxVsplit = 16;
 constexpr int kBK = 32;        // hidden-dimension depth per LDS stage: two 16-deep MFMA steps
 #ifndef ESTP_ENTROPY_STAGES
@@ -38,23 +37,31 @@ constexpr int kBK = 32;        // hidden-dimension depth per LDS stage: two 16-d
 #ifndef ESTP_ENTROPY_WAVES
 #define ESTP_ENTROPY_WAVES 8
 #endif
+#ifndef ESTP_ENTROPY_TILE_T
+#define ESTP_ENTROPY_TILE_T 256
+#endif
 constexpr int kStages = ESTP_ENTROPY_STAGES;  // LDS ring depth
-constexpr int kWaves = ESTP_ENTROPY_WAVES;    // 4 (one per SIMD) or 8 (two per SIMD)
+constexpr int kWaves = ESTP_ENTROPY_WAVES;    // waves per workgroup
+constexpr int kTileT = ESTP_ENTROPY_TILE_T;   // tokens per tile: 256 (one workgroup per CU) or 128 (two)
 
-// Geometry of one LDS stage (kBV rows of W then kBT rows of X, kBK bf16 each)
-// and of the wave layout: waves split the 256 x 256 tile 2 (vocabulary) x
+// Geometry of one LDS stage (kBV rows of W then BT rows of X, kBK bf16 each)
+// and of the wave layout: waves split the 256 x BT tile 2 (vocabulary) x
 // NW/2 (tokens); a wave owns 128 vocabulary rows x TW tokens.
-template <int NW>
+template <int NW, int BT>
 struct Geom {
+  static constexpr int kBT = BT;
   static constexpr int kThreads = NW * 64;
-  static constexpr int TW = 2 * kBT / NW;                           // tokens per wave: 128 or 64
+  static constexpr int TW = 2 * BT / NW;                            // tokens per wave: 128 or 64
   static constexpr int JT = TW / 32;                                // 32-token MFMA blocks per wave
   static constexpr int kRowBytes = kBK * 2;                         // 64 B
   static constexpr int kChunks = kRowBytes / 16;                    // 4 chunks of 16 B
   static constexpr int kRowsPerInst = 64 / kChunks;                 // 16 rows per wave instruction (1 KB)
-  static constexpr int kInstPerOperand = kBV / (kRowsPerInst * NW); // per wave per operand per stage
-  static constexpr int kLoadsPerStage = 2 * kInstPerOperand;        // vector-memory instructions per wave
-  static constexpr int kStageBytes = (kBV + kBT) * kRowBytes;       // 32 KB
+  static constexpr int kInstW = kBV / (kRowsPerInst * NW);          // W transfers per wave per stage
+  static constexpr int kInstX = BT / (kRowsPerInst * NW);           // X transfers per wave per stage
+  static constexpr int kLoadsPerStage = kInstW + kInstX;            // vector-memory instructions per wave
+  static constexpr int kStageBytes = (kBV + BT) * kRowBytes;
+  // workgroups that share a CU (LDS-limited), and so run together on one XCD
+  static constexpr int kWgPerCu = BT == 128 ? 2 : 1;
   static constexpr int kRowsPerWindow = 256 / kRowBytes;            // 4 rows share a 256-byte bank window
   // Chunk swizzle: the 16 rows that 16 consecutive lanes read at one logical
   // chunk land in 16 distinct 16-byte bank groups.
@@ -83,11 +90,12 @@ __device__ __forceinline__ void schedule_reads_front() {
   __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kGroups, 0);
 }
 
-template <int S, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
+template <int S, int NW, int BT>
+__global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
     int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
-  using G = Geom<NW>;
+  using G = Geom<NW, BT>;
+  constexpr int kBT = BT;
   constexpr int JT = G::JT;
   static_assert(S >= 3, "the ring needs at least three stages");
   __shared__ __attribute__((aligned(16))) char lds[S * G::kStageBytes];
@@ -102,11 +110,12 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
   int vs, tt;
   {
     const int bid = blockIdx.x;
-    if (n_vsplit == 16 && (n_tt % 16) == 0) {
+    constexpr int P = 32 * G::kWgPerCu;  // workgroups resident on one XCD
+    if (n_vsplit == 16 && (n_tt % (P / 2)) == 0) {
       const int xcd = bid & 7, j = bid >> 3;
-      const int wave_idx = j >> 5, jj = j & 31;
+      const int wave_idx = j / P, jj = j % P;
       vs = (xcd & 3) * 4 + (jj & 3);
-      tt = wave_idx * 16 + (xcd >> 2) * 8 + (jj >> 2);
+      tt = wave_idx * (P / 2) + (xcd >> 2) * (P / 4) + (jj >> 2);
     } else {
       vs = bid % n_vsplit;
       tt = bid / n_vsplit;
@@ -119,13 +128,16 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
 
   // ---- staging: lane l of instruction i fills row kRowsPerInst*(NW i + wave) + l / kChunks,
   // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.
-  int st_row[G::kInstPerOperand];
-  uint32_t st_chunk_off[G::kInstPerOperand], offx[G::kInstPerOperand];
+  int st_row[G::kInstW];
+  uint32_t st_chunk_off[G::kInstW], offx[G::kInstX];
   const char* xt = reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride;
 #pragma unroll
-  for (int i = 0; i < G::kInstPerOperand; ++i) {
+  for (int i = 0; i < G::kInstW; ++i) {
     st_row[i] = G::kRowsPerInst * (NW * i + wave) + lane / G::kChunks;
     st_chunk_off[i] = uint32_t(G::swz(st_row[i], lane % G::kChunks) * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < G::kInstX; ++i) {
     const int tr = min(tt * kBT + st_row[i], n_tok - 1) - tt * kBT;
     offx[i] = uint32_t(tr) * uint32_t(row_stride) + st_chunk_off[i];
   }
@@ -143,11 +155,11 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
     const char* wk = reinterpret_cast<const char*>(W) + size_t(vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
     const char* xk = xt + size_t(ks) * G::kRowBytes;
 #pragma unroll
-    for (int i = 0; i < G::kInstPerOperand; ++i) {
+    for (int i = 0; i < G::kInstW; ++i) {
       const int vr = min(vt * kBV + st_row[i], V - 1) - vt * kBV;
       char* dst = base + G::kRowsPerInst * (NW * i + wave) * G::kRowBytes;
       lds_dma16(wk + (uint32_t(vr) * uint32_t(row_stride) + st_chunk_off[i]), dst);
-      lds_dma16(xk + offx[i], dst + kBV * G::kRowBytes);
+      if (i < G::kInstX) lds_dma16(xk + offx[i], dst + kBV * G::kRowBytes);
     }
     ++pf_step;
     const bool wrap = pf_ks + 1 == nk;
@@ -287,7 +299,7 @@ __global__ __launch_bounds__(NW * 64, 1) void entropy_gemm_kernel(
   }
   // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS
   __syncthreads();  // every wave is done with the ring (no loads remain in flight)
-  float* xbuf = reinterpret_cast<float*>(lds);  // [256 tokens][3]
+  float* xbuf = reinterpret_cast<float*>(lds);  // [BT tokens][3]
   if (wv == 1 && frag_half == 0) {
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
@@ -375,7 +387,7 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
 
   const int n = int(n_tok);
   const int n_vt = (V + kBV - 1) / kBV;
-  const int n_tt = (n + kBT - 1) / kBT;
+  const int n_tt = (n + kTileT - 1) / kTileT;
   const int n_vsplit = choose_vsplit(n_vt);
   Carver c(workspace);
   float* pm = c.take<float>(size_t(n_vsplit) * n);
@@ -383,7 +395,7 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pt = c.take<float>(size_t(n_vsplit) * n);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  entropy_gemm_kernel<kStages, kWaves><<<dim3(n_vsplit * n_tt), dim3(Geom<kWaves>::kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+  entropy_gemm_kernel<kStages, kWaves, kTileT><<<dim3(n_vsplit * n_tt), dim3(Geom<kWaves, kTileT>::kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
   ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");

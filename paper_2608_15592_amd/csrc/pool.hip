@@ -1,26 +1,34 @@
 // Fusion and pooling, Eq. 3 - Eq. 5 (Section 4.2):
 //   T_i = lambda1 S_i + lambda2 H_i,  e_i = softmax_{prompt}(T_i / alpha),  h_b = sum_i e_i x_i
 //
-// combine_kernel: one workgroup per prompt computes the (optional) z-scores,
-// the max and exp-sum of T / alpha, writes e and the argmax token.  Traffic is
-// ~16 bytes per token.
-//
-// pool_partial_kernel: the bandwidth-bound part.  Workgroup (chunk, prompt,
-// d-slice) streams kChunk rows of X: each thread owns 8 consecutive hidden
-// features (one 16-byte load of bf16 per row), accumulates e_i * x_i in fp32
-// with 8 rows in flight, and writes one fp32 partial row.  pool_reduce_kernel
-// sums the chunk partials of each prompt in a fixed order (deterministic, no
-// atomics).
+// The weights are never normalised before pooling.  pool_partial_kernel
+// (workgroup = 256-token chunk x prompt x 2048-feature slice) forms
+// u_i = T_i / alpha for its rows, the chunk's own max m_c (and first arg-max),
+// p_i = exp(u_i - m_c) and exp-sum s_c with wave reductions only, and streams
+// X once: each thread owns 8 consecutive hidden features (one 16-byte bf16
+// load per row, 16 rows in flight) and accumulates sum_i p_i x_i in fp32.  pool_finish_kernel combines the chunks of each
+// prompt in a fixed order, weighting chunk c by exp(m_c - M) / Z (M the prompt
+// max, Z its exp-sum), which is exactly sum_i e_i x_i; it also writes the
+// arg-max token and, when asked, the normalised weights e.  With z-scored
+// inputs a per-prompt statistics pass (zscore_stats_kernel) runs first.  No
+// atomics: results are bitwise reproducible.
 #include "estp_common.h"
 
 namespace estp {
 namespace detail {
 
-constexpr int kCombineThreads = 1024;
-constexpr int kPoolThreads = 256;
-constexpr int kChunk = 256;                     // rows per pooling workgroup
-constexpr int kSlice = kPoolThreads * 8;        // hidden features per pooling workgroup
+constexpr int kThreads = 256;
+constexpr int kChunk = 256;                // rows per pooling workgroup (= threads of the weights kernel)
+constexpr int kSlice = kThreads * 8;       // hidden features per pooling workgroup
 constexpr float kZEps = 1e-6f;
+constexpr int kMaxChunks = 1024;           // chunks per prompt the finisher stages (prompts up to 256k tokens)
+
+struct ChunkStat {
+  float m;    // max of u over the chunk
+  float s;    // sum of 2^((u - m) log2 e) over the chunk
+  int idx;    // lowest row (prompt-local) attaining m
+  int pad;
+};
 
 __device__ float block_sum(float v, float* sh) {
   v = wave_sum(v);
@@ -34,7 +42,7 @@ __device__ float block_sum(float v, float* sh) {
   return r;
 }
 
-// (max value, lowest index attaining it)
+// (max value, lowest index attaining it) over the workgroup
 __device__ void block_argmax(float& v, int& idx, float* shv, int* shi) {
   for (int o = 32; o > 0; o >>= 1) {
     const float ov = __shfl_xor(v, o, 64);
@@ -61,144 +69,224 @@ __device__ void block_argmax(float& v, int& idx, float* shv, int* shi) {
     }
 }
 
-__global__ __launch_bounds__(kCombineThreads) void combine_kernel(const float* __restrict__ S,
-                                                                  const float* __restrict__ H,
-                                                                  const int* __restrict__ cu, float lambda1,
-                                                                  float lambda2, float inv_alpha, int zscore,
-                                                                  float* __restrict__ e, float* __restrict__ stats,
-                                                                  int* __restrict__ top) {
-  __shared__ float shv[kCombineThreads / 64];
-  __shared__ int shi[kCombineThreads / 64];
+// Per-prompt coefficients of u = a1 S + a2 H + c0 for z-scored inputs:
+// (lambda1 (S - mean_S) / (std_S + eps) + lambda2 (H - mean_H) / (std_H + eps)) / alpha.
+__global__ __launch_bounds__(1024) void zscore_stats_kernel(const float* __restrict__ S, const float* __restrict__ H,
+                                                            const int* __restrict__ cu, float a1, float a2,
+                                                            float4* __restrict__ coef) {
+  __shared__ float sh[16];
   const int b = blockIdx.x;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
-  const float* s = S + base;
-  const float* h = H + base;
-
-  // effective coefficients: T/alpha = a1 * S + a2 * H + const (const drops out of the softmax)
-  float a1 = lambda1 * inv_alpha, a2 = lambda2 * inv_alpha, c0 = 0.f;
-  if (zscore) {
-    float ss = 0.f, sh = 0.f;
-    for (int i = threadIdx.x; i < N; i += blockDim.x) {
-      ss += s[i];
-      sh += h[i];
-    }
-    const float ms = block_sum(ss, shv) / N;
-    const float mh = block_sum(sh, shv) / N;
-    float vs = 0.f, vh = 0.f;
-    for (int i = threadIdx.x; i < N; i += blockDim.x) {
-      vs += (s[i] - ms) * (s[i] - ms);
-      vh += (h[i] - mh) * (h[i] - mh);
-    }
-    const float sds = sqrtf(block_sum(vs, shv) / N);
-    const float sdh = sqrtf(block_sum(vh, shv) / N);
-    a1 /= (sds + kZEps);
-    a2 /= (sdh + kZEps);
-    c0 = -(a1 * ms + a2 * mh);
-  }
-  // u_i = T_i / alpha; max with lowest index
-  float mx = -INFINITY;
-  int mi = 0x7fffffff;
+  float ss = 0.f, sv = 0.f;
   for (int i = threadIdx.x; i < N; i += blockDim.x) {
-    const float u = fmaf(a1, s[i], fmaf(a2, h[i], c0));
-    if (u > mx) {
-      mx = u;
-      mi = i;
-    }
+    ss += S[base + i];
+    sv += H[base + i];
   }
-  block_argmax(mx, mi, shv, shi);
-  float z = 0.f;
-  for (int i = threadIdx.x; i < N; i += blockDim.x)
-    z += fast_exp2((fmaf(a1, s[i], fmaf(a2, h[i], c0)) - mx) * kLog2e);
-  const float Z = block_sum(z, shv);
-  const float invZ = 1.f / Z;
-  for (int i = threadIdx.x; i < N; i += blockDim.x)
-    e[base + i] = fast_exp2((fmaf(a1, s[i], fmaf(a2, h[i], c0)) - mx) * kLog2e) * invZ;
+  const float ms = block_sum(ss, sh) / N;
+  const float mh = block_sum(sv, sh) / N;
+  float vs = 0.f, vh = 0.f;
+  for (int i = threadIdx.x; i < N; i += blockDim.x) {
+    const float ds = S[base + i] - ms, dh = H[base + i] - mh;
+    vs += ds * ds;
+    vh += dh * dh;
+  }
+  const float sds = sqrtf(block_sum(vs, sh) / N);
+  const float sdh = sqrtf(block_sum(vh, sh) / N);
   if (threadIdx.x == 0) {
-    if (top) top[b] = base + mi;
-    if (stats) {
-      stats[2 * b] = mx;
-      stats[2 * b + 1] = Z;
-    }
+    const float c1 = a1 / (sds + kZEps), c2 = a2 / (sdh + kZEps);
+    coef[b] = make_float4(c1, c2, -(c1 * ms + c2 * mh), 0.f);
   }
 }
 
+// One row's 8 consecutive features as loaded (raw), and their fp32 values.
 template <typename T>
 struct Row8;
 template <>
 struct Row8<uint16_t> {  // 8 bf16 in one 16-byte load
-  __device__ static __forceinline__ void load(const uint16_t* p, float (&v)[8]) {
-    const uint4 q = *reinterpret_cast<const uint4*>(p);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  using Raw = uint4;
+  __device__ static __forceinline__ Raw load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ static __forceinline__ void fma8(float w, const Raw& q, float (&acc)[8]) {
+    const uint32_t x[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      v[2 * k] = __uint_as_float(w[k] << 16);
-      v[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+      acc[2 * k] = fmaf(w, __uint_as_float(x[k] << 16), acc[2 * k]);
+      acc[2 * k + 1] = fmaf(w, __uint_as_float(x[k] & 0xffff0000u), acc[2 * k + 1]);
     }
   }
 };
 template <>
 struct Row8<float> {  // 8 fp32 in two 16-byte loads
-  __device__ static __forceinline__ void load(const float* p, float (&v)[8]) {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  struct Raw {
+    float4 a, b;
+  };
+  __device__ static __forceinline__ Raw load(const float* p) {
+    return Raw{*reinterpret_cast<const float4*>(p), *reinterpret_cast<const float4*>(p + 4)};
+  }
+  __device__ static __forceinline__ void fma8(float w, const Raw& q, float (&acc)[8]) {
+    acc[0] = fmaf(w, q.a.x, acc[0]); acc[1] = fmaf(w, q.a.y, acc[1]);
+    acc[2] = fmaf(w, q.a.z, acc[2]); acc[3] = fmaf(w, q.a.w, acc[3]);
+    acc[4] = fmaf(w, q.b.x, acc[4]); acc[5] = fmaf(w, q.b.y, acc[5]);
+    acc[6] = fmaf(w, q.b.z, acc[6]); acc[7] = fmaf(w, q.b.w, acc[7]);
   }
 };
 
+__device__ __forceinline__ float4 coef_of(const float4* coef, int b, float a1, float a2) {
+  return coef ? coef[b] : make_float4(a1, a2, 0.f, 0.f);
+}
+
+// Streams one chunk of X.  Every wave forms the chunk's weights by itself
+// (wave reductions only, no workgroup barrier), so the first rows of X, which
+// do not depend on the weights, are already in flight while they are formed.
 template <typename T>
-__global__ __launch_bounds__(kPoolThreads) void pool_partial_kernel(const T* __restrict__ X,
-                                                                    const float* __restrict__ e,
-                                                                    const int* __restrict__ cu, int d,
-                                                                    int n_chunk_max, float* __restrict__ part) {
+__global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restrict__ X, const float* __restrict__ S,
+                                                                const float* __restrict__ H,
+                                                                const int* __restrict__ cu, int d, int n_chunk_max,
+                                                                float a1, float a2, const float4* __restrict__ coef,
+                                                                float* __restrict__ part,
+                                                                ChunkStat* __restrict__ cstat) {
+  __shared__ float wts[kThreads / 64][kChunk];  // one private copy of the chunk weights per wave
   const int chunk = blockIdx.x;
   const int b = blockIdx.y;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   const int r0 = chunk * kChunk;
   if (r0 >= N) return;
-  const int r1 = min(N, r0 + kChunk);
-  const int c = (blockIdx.z * kPoolThreads + threadIdx.x) * 8;
-  if (c >= d) return;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  const T* xp = X + size_t(base) * d + c;
-  const float* ep = e + base;
-  int r = r0;
-  for (; r + 8 <= r1; r += 8) {
-    float v[8][8];
+  const int nr = min(N - r0, kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = (blockIdx.z * kThreads + threadIdx.x) * 8;
+  const bool active = c < d;
+  const T* xp = X + size_t(base + r0) * d + (active ? c : 0);
+
+  constexpr int kInFlight = 16;
+  typename Row8<T>::Raw v[kInFlight];
+  const int n_first = min(nr, kInFlight);
+  if (active) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) Row8<T>::load(xp + size_t(r + k) * d, v[k]);
+    for (int k = 0; k < kInFlight; ++k)
+      if (k < n_first) v[k] = Row8<T>::load(xp + size_t(k) * d);
+  }
+
+  // u for rows lane, lane + 64, ...; wave-wide max (first arg-max), weights, sum
+  const float4 cf = coef_of(coef, b, a1, a2);
+  constexpr int kPer = kChunk / 64;
+  float u[kPer];
+  float m = -INFINITY;
+  int mi = 0x7fffffff;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float w = ep[r + k];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) acc[q] = fmaf(w, v[k][q], acc[q]);
+  for (int q = 0; q < kPer; ++q) {
+    const int r = q * 64 + lane;
+    u[q] = -INFINITY;
+    if (r < nr) {
+      const int i = base + r0 + r;
+      u[q] = fmaf(cf.x, S[i], fmaf(cf.y, H[i], cf.z));
+      if (u[q] > m) {  // rows visited in increasing order: strict keeps the first
+        m = u[q];
+        mi = r0 + r;
+      }
     }
   }
-  for (; r < r1; ++r) {
-    float v[8];
-    Row8<T>::load(xp + size_t(r) * d, v);
-    const float w = ep[r];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = fmaf(w, v[q], acc[q]);
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, 64);
+    const int oi = __shfl_xor(mi, o, 64);
+    if (om > m || (om == m && oi < mi)) {
+      m = om;
+      mi = oi;
+    }
   }
+  float sc = 0.f;
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const float p = fast_exp2((u[q] - m) * kLog2e);  // 0 for rows past the chunk (u = -inf)
+    wts[wave][q * 64 + lane] = p;
+    sc += p;
+  }
+  sc = wave_sum(sc);
+  if (threadIdx.x == 0 && blockIdx.z == 0) cstat[size_t(b) * n_chunk_max + chunk] = ChunkStat{m, sc, mi, 0};
+
+  if (!active) return;
+  const float* w = wts[wave];
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < kInFlight; ++k)
+    if (k < n_first) Row8<T>::fma8(w[k], v[k], acc);
+  int r = n_first;
+  for (; r + kInFlight <= nr; r += kInFlight) {
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k) v[k] = Row8<T>::load(xp + size_t(r + k) * d);
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k) Row8<T>::fma8(w[r + k], v[k], acc);
+  }
+  for (; r < nr; ++r) Row8<T>::fma8(w[r], Row8<T>::load(xp + size_t(r) * d), acc);
   float* out = part + (size_t(b) * n_chunk_max + chunk) * d + c;
   *reinterpret_cast<float4*>(out) = make_float4(acc[0], acc[1], acc[2], acc[3]);
   *reinterpret_cast<float4*>(out + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
 }
 
-__global__ __launch_bounds__(256) void pool_reduce_kernel(const float* __restrict__ part, const int* __restrict__ cu,
-                                                          int d, int n_chunk_max, float* __restrict__ pooled) {
+// Combine the chunks of prompt b in a fixed order:
+// pooled = sum_c 2^((m_c - M) log2 e) partial_c / Z,  Z = sum_c 2^((m_c - M) log2 e) s_c.
+// Workgroups x < nslices each finish a 2048-feature slice; the rest write the
+// normalised weights e of 1024 tokens each (when asked); x = 0 writes the top token.
+__global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __restrict__ part,
+                                                               const ChunkStat* __restrict__ cstat,
+                                                               const float* __restrict__ S,
+                                                               const float* __restrict__ H,
+                                                               const int* __restrict__ cu, int d, int n_chunk_max,
+                                                               int nslices, float a1, float a2,
+                                                               const float4* __restrict__ coef,
+                                                               float* __restrict__ pooled, float* __restrict__ e,
+                                                               int* __restrict__ top) {
+  __shared__ ChunkStat cs[kMaxChunks];
+  const int slice = blockIdx.x;
   const int b = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= d) return;
-  const int N = cu[b + 1] - cu[b];
+  const int base = cu[b];
+  const int N = cu[b + 1] - base;
   const int nch = (N + kChunk - 1) / kChunk;
-  const float* p = part + size_t(b) * n_chunk_max * d + c;
-  float v = 0.f;
-  for (int k = 0; k < nch; ++k) v += p[size_t(k) * d];
-  pooled[size_t(b) * d + c] = v;
+  for (int k = threadIdx.x; k < nch; k += kThreads) cs[k] = cstat[size_t(b) * n_chunk_max + k];
+  __syncthreads();
+  float M = -INFINITY;
+  int Mi = 0;
+  for (int k = 0; k < nch; ++k)
+    if (cs[k].m > M) {  // strict: the first chunk attaining the max keeps the lowest index
+      M = cs[k].m;
+      Mi = cs[k].idx;
+    }
+  float Z = 0.f;
+  for (int k = 0; k < nch; ++k) Z += cs[k].s * fast_exp2((cs[k].m - M) * kLog2e);
+  const float invZ = 1.f / Z;
+
+  if (slice >= nslices) {  // weights of tokens [1024 (slice - nslices), + 1024)
+    if (!e) return;
+    const float4 cf = coef_of(coef, b, a1, a2);
+    const int i1 = min(N, (slice - nslices + 1) * 1024);
+    for (int i = (slice - nslices) * 1024 + threadIdx.x; i < i1; i += kThreads) {
+      const float u = fmaf(cf.x, S[base + i], fmaf(cf.y, H[base + i], cf.z));
+      e[base + i] = fast_exp2((u - M) * kLog2e) * invZ;
+    }
+    return;
+  }
+  if (slice == 0 && top && threadIdx.x == 0) top[b] = base + Mi;
+  const int c = (slice * kThreads + threadIdx.x) * 8;
+  if (c < d) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const float* p = part + size_t(b) * n_chunk_max * d + c;
+    for (int k = 0; k < nch; ++k) {
+      const float w = fast_exp2((cs[k].m - M) * kLog2e) * invZ;
+      const float4 x0 = *reinterpret_cast<const float4*>(p + size_t(k) * d);
+      const float4 x1 = *reinterpret_cast<const float4*>(p + size_t(k) * d + 4);
+      acc[0] = fmaf(w, x0.x, acc[0]);
+      acc[1] = fmaf(w, x0.y, acc[1]);
+      acc[2] = fmaf(w, x0.z, acc[2]);
+      acc[3] = fmaf(w, x0.w, acc[3]);
+      acc[4] = fmaf(w, x1.x, acc[4]);
+      acc[5] = fmaf(w, x1.y, acc[5]);
+      acc[6] = fmaf(w, x1.z, acc[6]);
+      acc[7] = fmaf(w, x1.w, acc[7]);
+    }
+    float* out = pooled + size_t(b) * d + c;
+    *reinterpret_cast<float4*>(out) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    *reinterpret_cast<float4*>(out + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  }
 }
 
 }  // namespace detail
@@ -213,9 +301,9 @@ extern "C" size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int
   if (n_tok < 1 || B < 1 || max_seqlen < 1 || d < 1) return 0;
   const size_t nch = (size_t(max_seqlen) + kChunk - 1) / kChunk;
   Carver c(nullptr);
-  c.take<float>(size_t(n_tok));          // e (when the caller passes none)
-  c.take<float>(size_t(B) * 2);          // per-prompt (max, sum)
-  c.take<float>(size_t(B) * nch * d);    // chunk partials
+  c.take<float4>(size_t(B));            // per-prompt coefficients (z-score)
+  c.take<ChunkStat>(size_t(B) * nch);   // chunk statistics
+  c.take<float>(size_t(B) * nch * d);   // chunk partials
   return c.bytes();
 }
 
@@ -241,6 +329,8 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
                dtype);
   ESTP_REQUIRE(aligned(X, 16) && aligned(pooled, 16), ESTP_ERR_INVALID_ARG,
                "estp_combine_pool: X and pooled must be 16-byte aligned");
+  ESTP_REQUIRE(max_seqlen <= kMaxChunks * kChunk, ESTP_ERR_UNSUPPORTED,
+               "estp_combine_pool: prompts longer than %d tokens are not supported", kMaxChunks * kChunk);
   const size_t need = estp_combine_pool_workspace_size(n_tok, B, max_seqlen, d, dtype);
   ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
                "estp_combine_pool: workspace of %zu bytes, %zu needed", workspace_bytes, need);
@@ -248,23 +338,31 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
                "estp_combine_pool: workspace must be non-null and 256-byte aligned");
 
   const int nch = (max_seqlen + kChunk - 1) / kChunk;
+  const int nslices = (d + kSlice - 1) / kSlice;
   Carver c(workspace);
-  float* ews = c.take<float>(size_t(n_tok));
-  float* stats = c.take<float>(size_t(B) * 2);
+  float4* coef = c.take<float4>(size_t(B));
+  ChunkStat* cstat = c.take<ChunkStat>(size_t(B) * nch);
   float* part = c.take<float>(size_t(B) * nch * d);
-  float* ew = e ? e : ews;
+  const float a1 = lambda1 / alpha, a2 = lambda2 / alpha;
+  const float4* cf = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-
-  combine_kernel<<<dim3(B), dim3(kCombineThreads), 0, s>>>(S, H, cu_seqlens, lambda1, lambda2, 1.f / alpha, norm == ESTP_NORM_ZSCORE ? 1 : 0, ew, stats, top);
-  ESTP_CHECK_LAUNCH("combine_kernel");
-  const dim3 grid(nch, B, (d + kSlice - 1) / kSlice);
+  if (norm == ESTP_NORM_ZSCORE) {
+    zscore_stats_kernel<<<dim3(B), dim3(1024), 0, s>>>(S, H, cu_seqlens, a1, a2, coef);
+    ESTP_CHECK_LAUNCH("zscore_stats_kernel");
+    cf = coef;
+  }
+  const dim3 grid(nch, B, nslices);
   if (dtype == ESTP_BF16) {
-    pool_partial_kernel<uint16_t><<<grid, dim3(kPoolThreads), 0, s>>>(static_cast<const uint16_t*>(X), ew, cu_seqlens, int(d), nch, part);
+    pool_partial_kernel<uint16_t><<<grid, dim3(kThreads), 0, s>>>(static_cast<const uint16_t*>(X), S, H, cu_seqlens,
+                                                                  int(d), nch, a1, a2, cf, part, cstat);
   } else {
-    pool_partial_kernel<float><<<grid, dim3(kPoolThreads), 0, s>>>(static_cast<const float*>(X), ew, cu_seqlens, int(d), nch, part);
+    pool_partial_kernel<float><<<grid, dim3(kThreads), 0, s>>>(static_cast<const float*>(X), S, H, cu_seqlens, int(d),
+                                                               nch, a1, a2, cf, part, cstat);
   }
   ESTP_CHECK_LAUNCH("pool_partial_kernel");
-  pool_reduce_kernel<<<dim3((d + 255) / 256, B), dim3(256), 0, s>>>(part, cu_seqlens, int(d), nch, pooled);
-  ESTP_CHECK_LAUNCH("pool_reduce_kernel");
+  const int ne = e ? (max_seqlen + 1023) / 1024 : 0;
+  pool_finish_kernel<<<dim3(nslices + ne, B), dim3(kThreads), 0, s>>>(part, cstat, S, H, cu_seqlens, int(d), nch,
+                                                                      nslices, a1, a2, cf, pooled, e, top);
+  ESTP_CHECK_LAUNCH("pool_finish_kernel");
   return ESTP_OK;
 }
