@@ -22,7 +22,8 @@
 // workgroups resident on one XCD (ids are dealt round-robin over the 8 XCDs)
 // cover 4 vocabulary slices x 8 token tiles, and one dispatch wave of 256
 // covers 16 x 16: concurrent workgroups stream the same W and X tiles through
-// that XCD's L2.
+// that XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices
+// that hold one tile more than the others are spread over the XCDs.
 #include "estp_common.h"
 
 namespace estp {
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
     if (n_vsplit == 16 && (n_tt % (P / 2)) == 0) {
       const int xcd = bid & 7, j = bid >> 3;
       const int wave_idx = j / P, jj = j % P;
-      vs = (xcd & 3) * 4 + (jj & 3);
+      vs = (jj & 3) * 4 + (xcd & 3);
       tt = wave_idx * (P / 2) + (xcd >> 2) * (P / 4) + (jj >> 2);
     } else {
       vs = bid % n_vsplit;
@@ -248,45 +249,88 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
       schedule_reads_front<kReads, kMfma>();
     }
 
-    // ---- fold the finished tile into the running states, one 32 x 32 block at a
-    // time.  acc[i][j][r] is the logit of vocabulary row
-    // vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4 for token
-    // tt*256 + wt*TW + j*32 + frag_row.
+    // ---- fold the finished tile into the running states.  acc[i][j][r] is the
+    // logit of vocabulary row vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4
+    // for token tt*BT + wt*TW + j*32 + frag_row.
+    //
+    // The state (m, s, t) is kept relative to a reference m that is the running
+    // log-sum-exp after each tile (rebased so that s = 1).  Full tiles are then
+    // folded with 3 VALU ops and one exp2 per logit and no max pass; a tile whose
+    // logits exceed the reference by more than 2^64 in weight (or overflow) is
+    // refolded exactly with its own max.  The ragged last vocabulary tile always
+    // takes the exact, masked path.
     const int vt = vs + tile * n_vsplit;
     const int vbase = vt * kBV + wv * 128 + 4 * frag_half;
     const bool ragged = (vt + 1) * kBV > V;
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
       Ent2 e = st[j];
+      bool exact = ragged;
+      if (!ragged) {
+        if (tile == 0) {  // first tile: the tile's own max is the reference
+          float mx = acc[0][j][0];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float z[16];
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          z[r] = acc[i][j][r];
-          if (ragged && vbase + i * 32 + 8 * (r >> 2) + (r & 3) >= V) z[r] = -INFINITY;
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[i][j][r]);
+          e = Ent2{mx * kLog2e, 0.f, 0.f};
         }
-        float mx = z[0];
+        float s = e.s, t = e.t;
 #pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, z[r]);
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float dd = fmaf(acc[i][j][r], kLog2e, -e.m);
+            const float p = fast_exp2(dd);
+            s += p;
+            t = fmaf(p, dd, t);
+          }
+          __builtin_amdgcn_sched_barrier(0);  // block by block: bounds live copies
+        }
+        if (s <= 0x1p64f) {
+          e.s = s;
+          e.t = t;
+        } else {
+          exact = true;  // overflow (or a logit far above the reference): refold exactly
+        }
+      }
+      if (exact) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const bool live = !ragged || vbase + i * 32 + 8 * (r >> 2) + (r & 3) < V;
+            mx = live ? fmaxf(mx, acc[i][j][r]) : mx;
+          }
         const float mnew = fmaxf(e.m, mx * kLog2e);
         const float dl = fmaxf(e.m - mnew, kExp2Floor);
         const float f = fast_exp2(dl);
         float s = f * e.s;
         float t = f * (e.t + e.s * dl);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float dd = fmaxf(fmaf(z[r], kLog2e, -mnew), kExp2Floor);
-          const float p = fast_exp2(dd);
-          s += p;
-          t = fmaf(p, dd, t);
-        }
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            // dead rows enter as -inf: dd clamps to the floor and adds 0 * floor,
+            // also while mnew is still -inf (a lane with no live row yet)
+            const bool live = !ragged || vbase + i * 32 + 8 * (r >> 2) + (r & 3) < V;
+            const float dd = fmaxf(fmaf(live ? acc[i][j][r] : -INFINITY, kLog2e, -mnew), kExp2Floor);
+            const float p = fast_exp2(dd);
+            s += p;
+            t = fmaf(p, dd, t);
+          }
         e = Ent2{mnew, s, t};
-        __builtin_amdgcn_sched_barrier(0);  // fold block by block: bounds live accumulator copies
+      }
+      // rebase to the running log-sum-exp: m += log2 s, s = 1, t = t / s - log2 s
+      // (s >= 1 here: the reference never exceeds the largest logit seen, in base 2)
+      if (e.s > 0.f) {
+        const float dl = fast_log2(e.s);
+        e = Ent2{e.m + dl, 1.f, e.t / e.s - dl};
       }
       st[j] = e;
     }
-  }
+  }  // tile
 
   // ---- lanes l and l+32 hold the same tokens: merge them
 #pragma unroll
