@@ -30,40 +30,30 @@ namespace estp {
 namespace detail {
 
 constexpr int kBV = 256;       // vocabulary rows per tile
+constexpr int kBT = 256;       // tokens per tile
+constexpr int kWaves = 8;      // waves per workgroup, two per SIMD
 constexpr int kMaxVsplit = 16;
-constexpr int kBK = 32;        // hidden-dimension depth per LDS stage: two 16-deep MFMA steps
-#ifndef ESTP_ENTROPY_STAGES
-#define ESTP_ENTROPY_STAGES 4
-#endif
-#ifndef ESTP_ENTROPY_WAVES
-#define ESTP_ENTROPY_WAVES 8
-#endif
-#ifndef ESTP_ENTROPY_TILE_T
-#define ESTP_ENTROPY_TILE_T 256
-#endif
-constexpr int kStages = ESTP_ENTROPY_STAGES;  // LDS ring depth
-constexpr int kWaves = ESTP_ENTROPY_WAVES;    // waves per workgroup
-constexpr int kTileT = ESTP_ENTROPY_TILE_T;   // tokens per tile: 256 (one workgroup per CU) or 128 (two)
 
-// Geometry of one LDS stage (kBV rows of W then BT rows of X, kBK bf16 each)
-// and of the wave layout: waves split the 256 x BT tile 2 (vocabulary) x
-// NW/2 (tokens); a wave owns 128 vocabulary rows x TW tokens.
-template <int NW, int BT>
+// Geometry of one LDS stage (kBV rows of W then kBT rows of X, BK bf16 of the
+// hidden dimension each) and of the wave layout: waves split the 256 x 256
+// tile 2 (vocabulary) x 4 (tokens); a wave owns 128 vocabulary rows x 64 tokens.
+// BK = 64 makes every row of a stage one 128-byte run of global memory, which
+// the texture path fetches as a single request; BK = 32 (64-byte runs) serves
+// hidden sizes that are an odd multiple of 32.
+template <int BK>
 struct Geom {
-  static constexpr int kBT = BT;
-  static constexpr int kThreads = NW * 64;
-  static constexpr int TW = 2 * BT / NW;                            // tokens per wave: 128 or 64
+  static constexpr int kThreads = kWaves * 64;
+  static constexpr int TW = 2 * kBT / kWaves;                       // 64 tokens per wave
   static constexpr int JT = TW / 32;                                // 32-token MFMA blocks per wave
-  static constexpr int kRowBytes = kBK * 2;                         // 64 B
-  static constexpr int kChunks = kRowBytes / 16;                    // 4 chunks of 16 B
-  static constexpr int kRowsPerInst = 64 / kChunks;                 // 16 rows per wave instruction (1 KB)
-  static constexpr int kInstW = kBV / (kRowsPerInst * NW);          // W transfers per wave per stage
-  static constexpr int kInstX = BT / (kRowsPerInst * NW);           // X transfers per wave per stage
+  static constexpr int kSub = BK / 16;                              // 16-deep MFMA steps per stage
+  static constexpr int kRowBytes = BK * 2;                          // 64 or 128 B
+  static constexpr int kChunks = kRowBytes / 16;                    // 16-byte chunks per row
+  static constexpr int kRowsPerInst = 64 / kChunks;                 // rows per wave instruction (1 KB)
+  static constexpr int kInstW = kBV / (kRowsPerInst * kWaves);      // W transfers per wave per stage
+  static constexpr int kInstX = kBT / (kRowsPerInst * kWaves);      // X transfers per wave per stage
   static constexpr int kLoadsPerStage = kInstW + kInstX;            // vector-memory instructions per wave
-  static constexpr int kStageBytes = (kBV + BT) * kRowBytes;
-  // workgroups that share a CU (LDS-limited), and so run together on one XCD
-  static constexpr int kWgPerCu = BT == 128 ? 2 : 1;
-  static constexpr int kRowsPerWindow = 256 / kRowBytes;            // 4 rows share a 256-byte bank window
+  static constexpr int kPartBytes = kBV * kRowBytes;                // one operand of one stage (kBV == kBT)
+  static constexpr int kRowsPerWindow = 256 / kRowBytes;            // rows that share a 256-byte bank window
   // Chunk swizzle: the 16 rows that 16 consecutive lanes read at one logical
   // chunk land in 16 distinct 16-byte bank groups.
   __device__ static __forceinline__ int swz(int row, int chunk) {
@@ -91,15 +81,28 @@ __device__ __forceinline__ void schedule_reads_front() {
   __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kGroups, 0);
 }
 
-template <int S, int NW, int BT>
-__global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void entropy_gemm_kernel(
+// Ring of P part slots.  A stage (BK deep) has two parts, its W rows and its
+// X rows; part 2s + 0 / 2s + 1 (W / X of stage s) lives in slot (2s + o) % P.
+// Within a stage the wave runs kSub k steps, each reading the next step's
+// fragments while its MFMAs run.  Before the last k step every wave waits for
+// its own fragment reads (so stage s is no longer read) and for stage s + 1 to
+// have landed, then one barrier; after it the two freed slots take parts
+// 2s + P and 2s + P + 1.  With P odd the W part of a stage is issued one stage
+// before its X part, and about (P - 2) / 2 stages of loads are in flight
+// while a stage is consumed.
+template <int P, int BK, bool SPLIT>
+__global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
     int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
-  using G = Geom<NW, BT>;
-  constexpr int kBT = BT;
+  using G = Geom<BK>;
   constexpr int JT = G::JT;
-  static_assert(S >= 3, "the ring needs at least three stages");
-  __shared__ __attribute__((aligned(16))) char lds[S * G::kStageBytes];
+  static_assert(kBV == kBT, "W and X parts share one slot size");
+  static_assert(P >= 4, "the ring needs at least two stages");
+  static_assert(G::kSub >= 2, "the barrier sits between the last two k steps of a stage");
+  static_assert(G::kInstW == G::kInstX, "equal load counts per part");
+  static_assert(4 * G::JT >= 2 * G::kInstW, "one transfer per MFMA of a k step");
+  constexpr int L = G::kInstW;  // vector-memory instructions per wave per part
+  __shared__ __attribute__((aligned(16))) char lds[P * G::kPartBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -111,30 +114,29 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
   int vs, tt;
   {
     const int bid = blockIdx.x;
-    constexpr int P = 32 * G::kWgPerCu;  // workgroups resident on one XCD
-    if (n_vsplit == 16 && (n_tt % (P / 2)) == 0) {
+    constexpr int R = 32;  // workgroups resident on one XCD
+    if (n_vsplit == 16 && (n_tt % (R / 2)) == 0) {
       const int xcd = bid & 7, j = bid >> 3;
-      const int wave_idx = j / P, jj = j % P;
+      const int wave_idx = j / R, jj = j % R;
       vs = (jj & 3) * 4 + (xcd & 3);
-      tt = wave_idx * (P / 2) + (xcd >> 2) * (P / 4) + (jj >> 2);
+      tt = wave_idx * (R / 2) + (xcd >> 2) * (R / 4) + (jj >> 2);
     } else {
       vs = bid % n_vsplit;
       tt = bid / n_vsplit;
     }
   }
-  const int nk = d / kBK;
+  const int nk = d / BK;
   const int n_my_tiles = (n_vt - vs + n_vsplit - 1) / n_vsplit;
-  const int n_steps = n_my_tiles * nk;
   const size_t row_stride = size_t(d) * 2;  // bytes per row of W and X
 
-  // ---- staging: lane l of instruction i fills row kRowsPerInst*(NW i + wave) + l / kChunks,
+  // ---- staging: lane l of instruction i fills row kRowsPerInst*(kWaves i + wave) + l / kChunks,
   // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.
   int st_row[G::kInstW];
   uint32_t st_chunk_off[G::kInstW], offx[G::kInstX];
   const char* xt = reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride;
 #pragma unroll
   for (int i = 0; i < G::kInstW; ++i) {
-    st_row[i] = G::kRowsPerInst * (NW * i + wave) + lane / G::kChunks;
+    st_row[i] = G::kRowsPerInst * (kWaves * i + wave) + lane / G::kChunks;
     st_chunk_off[i] = uint32_t(G::swz(st_row[i], lane % G::kChunks) * 16);
   }
 #pragma unroll
@@ -143,38 +145,63 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
     offx[i] = uint32_t(tr) * uint32_t(row_stride) + st_chunk_off[i];
   }
 
-  // ---- prefetch: the loads of step pf_step = (pf_tile, pf_ks).  Steps past the
-  // end re-load the last stage into the slot being freed (never read), so every
-  // step issues exactly kLoadsPerStage loads per wave and the waits below are
-  // the same on every step; the loop body stays one basic block.
-  int pf_tile = 0, pf_ks = 0, pf_step = 0;
-  auto issue_next = [&]() {
-    const bool live = pf_tile < n_my_tiles;
-    const int vt = vs + (live ? pf_tile : n_my_tiles - 1) * n_vsplit;
-    const int ks = live ? pf_ks : nk - 1;
-    char* base = lds + (pf_step % S) * G::kStageBytes;
-    const char* wk = reinterpret_cast<const char*>(W) + size_t(vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
-    const char* xk = xt + size_t(ks) * G::kRowBytes;
-#pragma unroll
-    for (int i = 0; i < G::kInstW; ++i) {
-      const int vr = min(vt * kBV + st_row[i], V - 1) - vt * kBV;
-      char* dst = base + G::kRowsPerInst * (NW * i + wave) * G::kRowBytes;
-      lds_dma16(wk + (uint32_t(vr) * uint32_t(row_stride) + st_chunk_off[i]), dst);
-      if (i < G::kInstX) lds_dma16(xk + offx[i], dst + kBV * G::kRowBytes);
-    }
-    ++pf_step;
-    const bool wrap = pf_ks + 1 == nk;
-    pf_ks = wrap ? 0 : pf_ks + 1;
-    pf_tile = wrap ? pf_tile + 1 : pf_tile;
+  // ---- prefetch of parts in order 0, 1, 2, ...: part q is operand q % 2 of
+  // stage q / 2 = (tile, ks).  Parts past the end re-load the last stage into
+  // the slot being freed (never read), so every barrier issues exactly 2 L
+  // loads per wave and the waits below are the same on every stage; the loop
+  // body stays one basic block.
+  int pf_tile = 0, pf_ks = 0, pf_slot = 0, pf_op = 0;
+  // Source and destination of the next part; advances the part counters.
+  struct Part {
+    const char* src;  // W: start of the vocabulary tile's rows at depth ks; X: same for the token tile
+    char* dst;        // this wave's first 1 KB block of the slot
+    int vt;           // vocabulary tile (W parts)
   };
+  auto next_part = [&](int op) {
+    const bool live = pf_tile < n_my_tiles;
+    const int ks = live ? pf_ks : nk - 1;
+    Part p;
+    p.dst = lds + pf_slot * G::kPartBytes + G::kRowsPerInst * wave * G::kRowBytes;
+    p.vt = vs + (live ? pf_tile : n_my_tiles - 1) * n_vsplit;
+    if (op == 0) {
+      p.src = reinterpret_cast<const char*>(W) + size_t(p.vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
+    } else {
+      p.src = xt + size_t(ks) * G::kRowBytes;
+      const bool wrap = pf_ks + 1 == nk;
+      pf_ks = wrap ? 0 : pf_ks + 1;
+      pf_tile = wrap ? pf_tile + 1 : pf_tile;
+    }
+    pf_slot = pf_slot + 1 == P ? 0 : pf_slot + 1;
+    return p;
+  };
+  // Transfer i (of L) of a part: 1 KB, kRowsPerInst rows.
+  auto dma_one = [&](const Part& p, int op, int i) {
+    char* dst = p.dst + G::kRowsPerInst * kWaves * i * G::kRowBytes;
+    if (op == 0) {
+      const int vr = min(p.vt * kBV + st_row[i], V - 1) - p.vt * kBV;
+      lds_dma16(p.src + (uint32_t(vr) * uint32_t(row_stride) + st_chunk_off[i]), dst);
+    } else {
+      lds_dma16(p.src + offx[i], dst);
+    }
+  };
+  auto issue_part = [&]() {
+    const int op = pf_op;
+    const Part p = next_part(op);
+#pragma unroll
+    for (int i = 0; i < L; ++i) dma_one(p, op, i);
+    pf_op ^= 1;
+  };
+  // The two parts issued at every barrier: their operands are fixed, since an
+  // even number of parts precedes each barrier's pair.
+  constexpr int kOpA = P % 2, kOpB = kOpA ^ 1;
 
   // ---- fragment reads: lane (row r = lane % 32, half h = lane / 32) reads 8 bf16 at
   // k offset 16 kk + 8 h of row r of each 32-row block.
   const int frag_row = lane & 31;
   const int frag_half = lane >> 5;
-  uint32_t fa_off[2][4], fb_off[2][JT];  // byte offsets inside a stage, per k step
+  uint32_t fa_off[G::kSub][4], fb_off[G::kSub][JT];  // byte offsets inside a stage, per k step
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
+  for (int kk = 0; kk < G::kSub; ++kk) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int ra = wv * 128 + i * 32 + frag_row;
@@ -183,15 +210,16 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
       const int rb = wt * G::TW + j * 32 + frag_row;
-      fb_off[kk][j] = kBV * G::kRowBytes + rb * G::kRowBytes + G::swz(rb, kk * 2 + frag_half) * 16;
+      fb_off[kk][j] = rb * G::kRowBytes + G::swz(rb, kk * 2 + frag_half) * 16;
     }
   }
-  auto read_frags = [&](Frags<JT>& f, int slot, int kk) {
-    const char* base = lds + slot * G::kStageBytes;
+  auto read_frags = [&](Frags<JT>& f, int slot_w, int slot_x, int kk) {
+    const char* bw = lds + slot_w * G::kPartBytes;
+    const char* bx = lds + slot_x * G::kPartBytes;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(base + fa_off[kk][i]);
+    for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(bw + fa_off[kk][i]);
 #pragma unroll
-    for (int j = 0; j < JT; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(base + fb_off[kk][j]);
+    for (int j = 0; j < JT; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(bx + fb_off[kk][j]);
   };
   constexpr int kReads = 4 + JT;       // LDS reads per k step
   constexpr int kMfma = 4 * JT;        // MFMAs per k step
@@ -201,13 +229,34 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
 #pragma unroll
   for (int cb = 0; cb < JT; ++cb) st[cb] = Ent2{-INFINITY, 0.f, 0.f};
 
-  // ---- prologue: stages 0 .. S-2 in flight; wait for stage 0, read its first fragments
+  // ---- prologue: the first parts in flight; wait for stage 0, read its first fragments
+  constexpr int kPrologue = SPLIT ? P - 1 : P;
 #pragma unroll
-  for (int p = 0; p < S - 1; ++p) issue_next();
-  wait_vm<(S - 2) * G::kLoadsPerStage>();
+  for (int q = 0; q < kPrologue; ++q) issue_part();
+  wait_vm<(kPrologue - 2) * L>();
   lds_barrier();
-  Frags<JT> f0, f1;
-  read_frags(f0, 0, 0);
+  Frags<JT> f[2];
+  read_frags(f[0], 0, 1, 0);
+  int sw = 0;  // slot of the W part of the current stage; its X part is in sw + 1 (mod P)
+
+  // MFMAs of one k step with the L transfers of part p0 and then, if n1 > 0,
+  // those of part p1 threaded between them, one per MFMA, so a burst of
+  // transfers never holds the wave away from the matrix core.
+  auto mfma_with_dma = [&](f32x16_t(&acc)[4][JT], const Frags<JT>& cur, const Part& p0, int op0, const Part& p1,
+                           int op1, int n1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < JT; ++j) {
+        const int m = i * JT + j;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[i], cur.b[j], acc[i][j], 0, 0, 0);
+        if (m < L)
+          dma_one(p0, op0, m);
+        else if (m < L + n1)
+          dma_one(p1, op1, m - L);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  };
 
   for (int tile = 0; tile < n_my_tiles; ++tile) {
     f32x16_t acc[4][JT];
@@ -219,34 +268,49 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     for (int ks = 0; ks < nk; ++ks) {
-      const int step = tile * nk + ks;
-      const int slot = step % S;
-      // Phase A: k step 0 of this stage on f0 while the k step 1 fragments load.
-      read_frags(f1, slot, 1);
+      const int sx = sw + 1 == P ? 0 : sw + 1;
+      const int sw_next = sx + 1 == P ? 0 : sx + 1;
+      const int sx_next = sw_next + 1 == P ? 0 : sw_next + 1;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int u = 0; u < G::kSub; ++u) {
+        Frags<JT>& cur = f[u & 1];
+        Frags<JT>& nxt = f[(u + 1) & 1];
+        if (u + 1 < G::kSub) {
+          read_frags(nxt, sw, sx, u + 1);
+          if (SPLIT && u == 0) {
+            // the second part freed at the previous barrier goes out here
+            const Part pb = next_part(kOpB);
+            mfma_with_dma(acc, cur, pb, kOpB, pb, kOpB, 0);
+            continue;
+          }
+        } else {
+          // This wave's reads of the stage are done (lgkmcnt 0 inside the
+          // barrier) and the next stage has landed (only the P - 4 parts
+          // issued after it may still be in flight): after the barrier nobody
+          // reads this stage's slots again, so they take the next two parts.
+          // The previous k step's MFMAs stay in front of the wait.
+          __builtin_amdgcn_sched_barrier(0);
+          wait_vm<(P - 4) * L>();
+          lds_barrier();
+          const Part pa = next_part(kOpA);
+          if (SPLIT) {
+            read_frags(nxt, sw_next, sx_next, 0);  // past the last stage: read and never used
+            mfma_with_dma(acc, cur, pa, kOpA, pa, kOpA, 0);
+          } else {
+            const Part pb = next_part(kOpB);
+            read_frags(nxt, sw_next, sx_next, 0);  // past the last stage: read and never used
+            mfma_with_dma(acc, cur, pa, kOpA, pb, kOpB, L);
+          }
+          continue;
+        }
 #pragma unroll
-        for (int j = 0; j < JT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[i], f0.b[j], acc[i][j], 0, 0, 0);
-      schedule_reads_front<kReads, kMfma>();
-
-      // Stage step+1 must be in LDS before anyone reads it; after this barrier
-      // every wave has also finished with slot (step-1) % S, which the next
-      // prefetch overwrites.  Issued after stage step+1: S-3 stages.
-      // Every read of slot (step-1) % S fed an MFMA of step step-1 already.
-      wait_vm<(S - 3) * G::kLoadsPerStage>();
-      ring_barrier();
-
-      // Phase B: k step 1 on f1 while the next stage's first fragments load and
-      // the prefetch of stage step+S-1 is issued.
-      read_frags(f0, (step + 1) % S, 0);  // past the last step: read and never used
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < JT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[i], f1.b[j], acc[i][j], 0, 0, 0);
-      issue_next();
-      schedule_reads_front<kReads, kMfma>();
+          for (int j = 0; j < JT; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[i], cur.b[j], acc[i][j], 0, 0, 0);
+        schedule_reads_front<kReads, kMfma>();
+      }
+      sw = sw_next;
     }
 
     // ---- fold the finished tile into the running states.  acc[i][j][r] is the
@@ -260,8 +324,8 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
     // refolded exactly with its own max.  The ragged last vocabulary tile always
     // takes the exact, masked path.
     const int vt = vs + tile * n_vsplit;
-    const int vbase = vt * kBV + wv * 128 + 4 * frag_half;
     const bool ragged = (vt + 1) * kBV > V;
+    const int lim = V - (vt * kBV + wv * 128 + 4 * frag_half);  // live rows: offset < lim
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
       Ent2 e = st[j];
@@ -300,7 +364,7 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const bool live = !ragged || vbase + i * 32 + 8 * (r >> 2) + (r & 3) < V;
+            const bool live = !ragged || i * 32 + 8 * (r >> 2) + (r & 3) < lim;
             mx = live ? fmaxf(mx, acc[i][j][r]) : mx;
           }
         const float mnew = fmaxf(e.m, mx * kLog2e);
@@ -314,7 +378,7 @@ __global__ __launch_bounds__(NW * 64, (NW * Geom<NW, BT>::kWgPerCu / 4)) void en
           for (int r = 0; r < 16; ++r) {
             // dead rows enter as -inf: dd clamps to the floor and adds 0 * floor,
             // also while mnew is still -inf (a lane with no live row yet)
-            const bool live = !ragged || vbase + i * 32 + 8 * (r >> 2) + (r & 3) < V;
+            const bool live = !ragged || i * 32 + 8 * (r >> 2) + (r & 3) < lim;
             const float dd = fmaxf(fmaf(live ? acc[i][j][r] : -INFINITY, kLog2e, -mnew), kExp2Floor);
             const float p = fast_exp2(dd);
             s += p;
@@ -417,8 +481,8 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG,
                "estp_token_entropy: unknown dtype %d", dtype);
   ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED, "estp_token_entropy: only ESTP_BF16 inputs are supported");
-  ESTP_REQUIRE(d % kBK == 0, ESTP_ERR_UNSUPPORTED,
-               "estp_token_entropy: d must be a multiple of %d for the matrix-core path, got %d", kBK, d);
+  ESTP_REQUIRE(d % 32 == 0, ESTP_ERR_UNSUPPORTED,
+               "estp_token_entropy: d must be a multiple of 32 for the matrix-core path, got %d", d);
   ESTP_REQUIRE(size_t(d) * 2 * kBV < (size_t(1) << 32), ESTP_ERR_UNSUPPORTED,
                "estp_token_entropy: d = %d too large", d);
   ESTP_REQUIRE(aligned(X, 16) && aligned(W, 16), ESTP_ERR_INVALID_ARG,
@@ -431,7 +495,7 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
 
   const int n = int(n_tok);
   const int n_vt = (V + kBV - 1) / kBV;
-  const int n_tt = (n + kTileT - 1) / kTileT;
+  const int n_tt = (n + kBT - 1) / kBT;
   const int n_vsplit = choose_vsplit(n_vt);
   Carver c(workspace);
   float* pm = c.take<float>(size_t(n_vsplit) * n);
@@ -439,7 +503,13 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pt = c.take<float>(size_t(n_vsplit) * n);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  entropy_gemm_kernel<kStages, kWaves, kTileT><<<dim3(n_vsplit * n_tt), dim3(Geom<kWaves, kTileT>::kThreads), 0, s>>>(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(W), n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+  const dim3 grid(n_vsplit * n_tt), block(kWaves * 64);
+  const uint16_t* Xh = static_cast<const uint16_t*>(X);
+  const uint16_t* Wh = static_cast<const uint16_t*>(W);
+  if (d % 64 == 0)
+    entropy_gemm_kernel<5, 64, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+  else
+    entropy_gemm_kernel<7, 32, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
   ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");

@@ -51,6 +51,10 @@ ENTROPY_CASES = [
     (256, 4096, 32768, 0.02, "llama-width-16-slices"),
     (200, 256, 3000, 1.5, "sharp-logits"),
     (64, 128, 600, 0.0, "uniform-logits"),
+    # widths that are an odd multiple of 32 take the 32-deep staging
+    (77, 32, 1300, 0.02, "width-32"),
+    (300, 96, 2500, 0.02, "width-96-ragged"),
+    (130, 4128, 3000, 0.02, "width-4128"),
 ]
 
 
