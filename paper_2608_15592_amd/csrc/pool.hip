@@ -6,7 +6,7 @@
 // u_i = T_i / alpha for its rows, the chunk's own max m_c (and first arg-max),
 // p_i = exp(u_i - m_c) and exp-sum s_c with wave reductions only, and streams
 // X once: each thread owns 8 consecutive hidden features (one 16-byte bf16
-// load per row, 16 rows in flight) and accumulates sum_i p_i x_i in fp32.  pool_finish_kernel combines the chunks of each
+// load per row, 8 rows in flight) and accumulates sum_i p_i x_i in fp32.  pool_finish_kernel combines the chunks of each
 // prompt in a fixed order, weighting chunk c by exp(m_c - M) / Z (M the prompt
 // max, Z its exp-sum), which is exactly sum_i e_i x_i; it also writes the
 // arg-max token and, when asked, the normalised weights e.  With z-scored
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
   const bool active = c < d;
   const T* xp = X + size_t(base + r0) * d + (active ? c : 0);
 
-  constexpr int kInFlight = 16;
+  constexpr int kInFlight = 8;
   typename Row8<T>::Raw v[kInFlight];
   const int n_first = min(nr, kInFlight);
   if (active) {

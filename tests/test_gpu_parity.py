@@ -185,6 +185,33 @@ def test_combine_pool_special_cases():
         assert rel_l2(host(pooled)[b], Xw[0]) <= 1e-6
 
 
+def test_combine_pool_slices_and_reused_workspace():
+    # three feature slices (the last one ragged), a prompt of many chunks, and one
+    # workspace shared by consecutive calls (its arrival counters must come back clean)
+    lengths = [5000, 3, 1300]
+    n = sum(lengths)
+    d = 4616
+    g = np.random.default_rng(10)
+    X = _bf16(g.standard_normal((n, d)).astype(np.float32))
+    S = (g.random(n) / 20).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    Xd, Sd, Hd, cud = dev(X), dev(S), dev(Hh), dev(cu)
+    nb = estp.load().estp_combine_pool_workspace_size(n, len(lengths), max(lengths), d, 0)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    for l1, l2, a, norm in [(0.5, 0.5, 1.0, "none"), (0.9, 0.1, 0.5, "zscore"), (0.2, 0.8, 2.0, "none")]:
+        pooled, e, top = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm, workspace=ws)
+        e_ref, _ = oracle.combine_weights(S, Hh, cu, l1, l2, a, norm)
+        p_ref = oracle.pool(X, e_ref, cu)
+        np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+        P = host(pooled)
+        top = host(top)
+        for b in range(len(lengths)):
+            assert rel_l2(P[b], p_ref[b]) <= POOL_RTOL
+            lo, hi = cu[b], cu[b + 1]
+            check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
+
+
 # ------------------------------------------------------------------------------------------ length head
 
 @pytest.mark.parametrize("K,act,B,d,Hdn", [(1, "relu", 37, 256, 96), (8, "relu", 37, 256, 96),
