@@ -19,7 +19,9 @@
 // each 32 x 32 block; 2^(c s - lse2) is summed per lane into column sums.
 // Partial column masses per (layer, KV head) are reduced in a fixed order by
 // attn_reduce_kernel, which divides by N * Hq.  No atomics: results are
-// bitwise reproducible.
+// bitwise reproducible.  Both passes are register-bounded to three waves per
+// SIMD (168 VGPRs, no spills) so that one wave's exponentials overlap the
+// others' matrix-core work.
 #include "estp_common.h"
 
 namespace estp {
@@ -62,7 +64,7 @@ __device__ __forceinline__ void stage_rows(char* dst, int rows, int wave, int nw
 
 // ---------------------------------------------------------------- pass 1
 template <int DH>
-__global__ __launch_bounds__(kThreads) void attn_lse_kernel(const uint16_t* __restrict__ Q,
+__global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* __restrict__ Q,
                                                             const uint16_t* __restrict__ K,
                                                             const int* __restrict__ cu, int B, int n_tok,
                                                             int L, int Hq, int Hkv, int nqb_max, float c2,
@@ -137,6 +139,11 @@ __global__ __launch_bounds__(kThreads) void attn_lse_kernel(const uint16_t* __re
       }
     }
     // acc[rb][cb][r]: key k0 + rb*32 + 8*(r/4) + 4*half + r%4, query q0 + cb*32 + col
+    // Running state per query column: reference m (base-2 units) and
+    // s = sum 2^(c2 s_ij - m).  After the first tile m is rebased to the
+    // running log-sum-exp (s = 1), so later tiles fold with one FMA, one exp2
+    // and one add per score and no max pass; a tile that would push s past
+    // 2^64 (or a lane with no reference yet) is refolded exactly with its max.
     const bool diag = k0 + kKTile - 1 > q0;
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
@@ -148,20 +155,33 @@ __global__ __launch_bounds__(kThreads) void attn_lse_kernel(const uint16_t* __re
           for (int r = 0; r < 16; ++r)
             if (k0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) > qi) acc[rb][cb][r] = -INFINITY;
       }
-      float mx = acc[0][cb][0];
+      float sum = s[cb];
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
-      const float mnew = fmaxf(m[cb], mx * c2);
-      float sum = s[cb] * fast_exp2(fmaxf(m[cb] - mnew, kExp2Floor));
+        for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[rb][cb][r], c2, -m[cb]));
+      if (!(sum <= 0x1p64f)) {  // overflow, NaN from m = -inf, or far above the reference
+        float mx = acc[0][cb][0];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[rb][cb][r], c2, -mnew));
-      // nothing seen yet in this lane (all keys masked): fmaf(-inf, c2, inf) is NaN, keep the empty state
-      s[cb] = (mnew == -INFINITY) ? 0.f : sum;
-      m[cb] = mnew;
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
+        const float mnew = fmaxf(m[cb], mx * c2);
+        sum = s[cb] * fast_exp2(fmaxf(m[cb] - mnew, kExp2Floor));
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[rb][cb][r], c2, -mnew));
+        // nothing seen yet in this lane (all keys masked): fmaf(-inf, c2, inf) is NaN, keep the empty state
+        sum = (mnew == -INFINITY) ? 0.f : sum;
+        m[cb] = mnew;
+      }
+      // rebase to the running log-sum-exp (s >= 1 whenever anything was seen)
+      if (sum > 0.f) {
+        m[cb] += fast_log2(sum);
+        sum = 1.f;
+      }
+      s[cb] = sum;
     }
   }
   // lanes col and col + 32 hold the two row quads of the same query column
@@ -178,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void attn_lse_kernel(const uint16_t* __re
 
 // ---------------------------------------------------------------- pass 2
 template <int DH>
-__global__ __launch_bounds__(kThreads) void attn_colsum_kernel(const uint16_t* __restrict__ Q,
+__global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t* __restrict__ Q,
                                                                const uint16_t* __restrict__ K,
                                                                const int* __restrict__ cu, int B, int n_tok,
                                                                int L, int Hq, int Hkv, float c2,
