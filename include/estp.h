@@ -131,6 +131,29 @@ ESTP_API int estp_attn_importance(const void* Q, const void* K, const int32_t* c
                          float* S, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Attention importance from a prefill's row normalisers (Eq. 1, Section 4.1).
+ *
+ * The same S as estp_attn_importance, with the first pass replaced by the
+ * caller's per-row log partition sums, as a FlashAttention-style prefill
+ * already returns them alongside its output:
+ *
+ *   lse [L, Hq, n_tok]  float32, natural log, device:
+ *                       lse[l][h][i] = log sum_{j <= i, same prompt} exp(scale q^{l,h}_i . k^{l,g(h)}_j)
+ *
+ * Row i of head h is then normalised as exp(scale q.k - lse[l][h][i]); the
+ * scores are formed once (the column-sum pass) instead of twice.  Values of
+ * lse that are not the exact normalisers give the correspondingly scaled
+ * rows (no renormalisation).  Other arguments, layouts and requirements are
+ * those of estp_attn_importance; `lse` must be non-null.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_attn_importance_from_lse_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L,
+                                                    int32_t Hq, int32_t Hkv, int32_t dh, int dtype);
+ESTP_API int estp_attn_importance_from_lse(const void* Q, const void* K, const float* lse, const int32_t* cu_seqlens,
+                                  int32_t B, int32_t max_seqlen, int64_t n_tok, int32_t L, int32_t Hq, int32_t Hkv,
+                                  int32_t dh, float scale, int dtype, float* S, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Fusion and pooling (Eq. 3, Eq. 4, Eq. 5, Section 4.2).
  *
  *   T_i = lambda1 S_i + lambda2 H_i              (after `norm`, per prompt)

@@ -10,7 +10,9 @@ exactly to float64 and evaluates the paper's definitions:
 
 * ``token_entropy``      - Eq. 2 (Section 4.2)
 * ``attn_importance``    - Eq. 1 (Section 4.1); ``attn_importance_tail``
-  gives the same S_j for the last m keys of one prompt from its last m rows
+  gives the same S_j for the last m keys of one prompt from its last m rows;
+  ``attn_row_lse`` is the log normaliser of every attention row and
+  ``attn_importance_from_lse`` forms S_j from given row normalisers
 * ``combine_weights``    - Eq. 3 and Eq. 4 (Section 4.2)
 * ``pool``               - Eq. 5 (Section 4.2)
 * ``predict``            - the MLP length head with Eq. 7 (Section 4.3)
@@ -25,6 +27,8 @@ from .estp_oracle import (  # noqa: F401
     token_entropy,
     attn_importance,
     attn_importance_tail,
+    attn_row_lse,
+    attn_importance_from_lse,
     combine_weights,
     pool,
     predict,

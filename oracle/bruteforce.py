@@ -85,3 +85,38 @@ def pooled(X, e, lengths):
         out.append([math.fsum(e[start + i] * _f(X[start + i][c]) for i in range(N)) for c in range(d)])
         start += N
     return out
+
+
+def row_lse(Q, K, lengths, scale):
+    """lse[h][t] = log sum_{j <= i} exp(scale q_i . k_j) for token t = start + i of each prompt (one layer)."""
+    Hq = len(Q[0])
+    G = Hq // len(K[0])
+    out = [[0.0] * len(Q) for _ in range(Hq)]
+    start = 0
+    for N in lengths:
+        for h in range(Hq):
+            for i in range(N):
+                s = [scale * math.fsum(_f(Q[start + i][h][c]) * _f(K[start + j][h // G][c]) for c in range(len(Q[0][0])))
+                     for j in range(i + 1)]
+                smax = max(s)
+                out[h][start + i] = smax + math.log(math.fsum(math.exp(v - smax) for v in s))
+        start += N
+    return out
+
+
+def importance_with_lse(Q, K, lengths, scale, lse):
+    """S for one layer with attention rows exp(s_ij - lse[h][t_i]) (Eq. 1 with given row normalisers)."""
+    Hq = len(Q[0])
+    G = Hq // len(K[0])
+    S = []
+    start = 0
+    for N in lengths:
+        for j in range(N):
+            terms = []
+            for h in range(Hq):
+                for i in range(j, N):
+                    s = scale * math.fsum(_f(Q[start + i][h][c]) * _f(K[start + j][h // G][c]) for c in range(len(Q[0][0])))
+                    terms.append(math.exp(s - lse[h][start + i]) / Hq)
+            S.append(math.fsum(terms) / N)
+        start += N
+    return S

@@ -121,6 +121,82 @@ def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: 
     return S
 
 
+def attn_row_lse(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: int = 2048) -> np.ndarray:
+    """Log partition sum of every causal attention row, [L, Hq, n_tok] (natural log).
+
+    lse_{l,h,i} = log sum_{j <= i, j in i's prompt} exp(scale q_i . k_j), the
+    normaliser of A_ij in Eq. 1 (Section 4.1) and what a FlashAttention-style
+    prefill returns per query row.
+    """
+    Qd = widen(Q)
+    Kd = widen(K)
+    if Qd.ndim == 3:
+        Qd, Kd = Qd[None], Kd[None]
+    L, n_tok, Hq, dh = Qd.shape
+    G = Hq // Kd.shape[2]
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    out = np.empty((L, Hq, n_tok), dtype=np.float64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        N = hi - lo
+        if N <= 0:
+            continue
+        j = np.arange(N)[None, :]
+        for l in range(L):
+            for h in range(Hq):
+                q = Qd[l, lo:hi, h, :]
+                k = Kd[l, lo:hi, h // G, :]
+                for i0 in range(0, N, row_chunk):
+                    s = scale * (q[i0:i0 + row_chunk] @ k.T)
+                    i = np.arange(i0, i0 + s.shape[0])[:, None]
+                    s = np.where(j <= i, s, -np.inf)
+                    m = s.max(axis=1)
+                    out[l, h, lo + i0:lo + i0 + s.shape[0]] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    return out
+
+
+def attn_importance_from_lse(Q, K, cu_seqlens, lse, scale: Optional[float] = None,
+                             row_chunk: int = 2048) -> np.ndarray:
+    """S_j of Eq. 1 with row i of every head normalised by the given ``lse`` [L, Hq, n_tok]:
+    A_ij = exp(scale q_i . k_j - lse_i) for j <= i, then averaged over heads,
+    summed over i and divided by N as in ``attn_importance``.  With
+    ``lse = attn_row_lse(...)`` the rows are the causal softmax rows and the
+    result is ``attn_importance``.
+    """
+    Qd = widen(Q)
+    Kd = widen(K)
+    lse = np.asarray(lse, dtype=np.float64)
+    if Qd.ndim == 3:
+        Qd, Kd = Qd[None], Kd[None]
+        lse = lse[None] if lse.ndim == 2 else lse
+    L, n_tok, Hq, dh = Qd.shape
+    G = Hq // Kd.shape[2]
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    S = np.zeros(n_tok, dtype=np.float64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        N = hi - lo
+        if N <= 0:
+            continue
+        j = np.arange(N)[None, :]
+        for l in range(L):
+            colsum = np.zeros(N, dtype=np.float64)
+            for h in range(Hq):
+                q = Qd[l, lo:hi, h, :]
+                k = Kd[l, lo:hi, h // G, :]
+                for i0 in range(0, N, row_chunk):
+                    s = scale * (q[i0:i0 + row_chunk] @ k.T)
+                    i = np.arange(i0, i0 + s.shape[0])[:, None]
+                    A = np.where(j <= i, np.exp(s - lse[l, h, lo + i0:lo + i0 + s.shape[0]][:, None]), 0.0)
+                    colsum += A.sum(axis=0) / Hq
+            S[lo:hi] += colsum / N
+    return S
+
+
 def attn_importance_tail(Q, K, N: int, m: int, scale: Optional[float] = None) -> np.ndarray:
     """S_j of Eq. 1 for the last ``m`` keys j = N-m .. N-1 of ONE prompt of length N.
 

@@ -27,6 +27,7 @@ EXPORTS = (
     "estp_version", "estp_status_string", "estp_last_error",
     "estp_token_entropy_workspace_size", "estp_token_entropy",
     "estp_attn_importance_workspace_size", "estp_attn_importance",
+    "estp_attn_importance_from_lse_workspace_size", "estp_attn_importance_from_lse",
     "estp_combine_pool_workspace_size", "estp_combine_pool",
     "estp_predict_workspace_size", "estp_predict",
 )
@@ -71,6 +72,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_attn_importance.restype = _INT
     lib.estp_attn_importance.argtypes = [_P, _P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _I32, _F, _INT, _P, _P,
                                          _SZ, _P]
+    lib.estp_attn_importance_from_lse_workspace_size.restype = _SZ
+    lib.estp_attn_importance_from_lse_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _I32, _I32, _I32, _INT]
+    lib.estp_attn_importance_from_lse.restype = _INT
+    lib.estp_attn_importance_from_lse.argtypes = [_P, _P, _P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _I32, _F,
+                                                  _INT, _P, _P, _SZ, _P]
     lib.estp_combine_pool_workspace_size.restype = _SZ
     lib.estp_combine_pool_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _INT]
     lib.estp_combine_pool.restype = _INT
@@ -186,6 +192,44 @@ def attn_importance(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, 
     _check(lib.estp_attn_importance(_ptr(Q), _ptr(K), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L, Hq, Hkv, dh,
                                     float(scale), dt, _ptr(S), _ptr(workspace), wsb, _stream(stream)),
            "estp_attn_importance")
+    return S
+
+
+def attn_importance_from_lse(Q: torch.Tensor, K: torch.Tensor, lse: torch.Tensor, cu_seqlens: torch.Tensor,
+                             max_seqlen: int, scale: Optional[float] = None, S: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Eq. 1 importance from given per-row natural-log normalisers ``lse`` [L, Hq, n_tok] (a prefill's LSE).
+
+    Q [L, n_tok, Hq, dh], K [L, n_tok, Hkv, dh] (3-D tensors and a 2-D ``lse`` are one layer).
+    """
+    lib = load()
+    if Q.dim() == 3:
+        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
+    if lse.dim() == 2:
+        lse = lse.unsqueeze(0)
+    _need(Q, "Q", ndim=4)
+    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
+    _need(lse, "lse", device=Q.device, dtype=torch.float32, ndim=3)
+    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
+    L, n_tok, Hq, dh = Q.shape
+    Hkv = K.shape[2]
+    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
+        raise ValueError("Q and K shapes disagree")
+    if tuple(lse.shape) != (L, Hq, n_tok):
+        raise ValueError(f"lse must be [L, Hq, n_tok] = {(L, Hq, n_tok)}, got {tuple(lse.shape)}")
+    B = cu_seqlens.numel() - 1
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    if S is None:
+        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+    _need(S, "S", device=Q.device, dtype=torch.float32)
+    dt = _dtype_code(Q)
+    ws = lib.estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
+    workspace, wsb = _workspace(ws, Q.device, workspace)
+    _check(lib.estp_attn_importance_from_lse(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok,
+                                             L, Hq, Hkv, dh, float(scale), dt, _ptr(S), _ptr(workspace), wsb,
+                                             _stream(stream)),
+           "estp_attn_importance_from_lse")
     return S
 
 

@@ -33,7 +33,7 @@ constexpr int kQBlock = 4 * kQPerWave;
 constexpr int kKPerWave = 64;  // keys per wave in pass 2
 constexpr int kKBlock = 4 * kKPerWave;
 constexpr int kKTile = 64;     // keys per streamed tile in pass 1
-constexpr int kQTile = 32;     // queries per streamed tile in pass 2
+constexpr int kQTile = 32;     // queries per streamed tile in pass 2 (64 spills or costs a wave)
 
 // Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
 // consecutive rows read at one logical chunk hit 16 distinct bank groups.
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
                                                                const uint16_t* __restrict__ K,
                                                                const int* __restrict__ cu, int B, int n_tok,
                                                                int L, int Hq, int Hkv, float c2,
-                                                               const float* __restrict__ lse2,
+                                                               const float* __restrict__ lse2, float lse_mul,
                                                                float* __restrict__ part) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
@@ -253,10 +253,10 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
     stage_rows<DH>(qtile[buf], kQTile, wave, 4, lane,
                    [&](int r) { return Ql + size_t(min(qb * kQTile + r, N - 1)) * qrow + size_t(hh) * DH; });
   };
-  auto lse_load = [&](int t) {  // lanes 0..31 of wave 0 fetch the tile's 32 row LSEs
+  auto lse_load = [&](int t) {  // lanes below kQTile of wave 0 fetch the tile's row LSEs
     const int hh = g * G + t % G;
     const int i = (qb_first + t / G) * kQTile + lane;
-    return (lane < kQTile && i < N) ? Ll[size_t(hh) * n_tok + i] : INFINITY;  // rows past N weigh 0
+    return (lane < kQTile && i < N) ? Ll[size_t(hh) * n_tok + i] * lse_mul : INFINITY;  // rows past N weigh 0
   };
 
   stage(0, 0);
@@ -274,46 +274,55 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
     const int i0 = qb * kQTile;
     if (i0 + kQTile - 1 >= k0 && k0 < N) {  // some query of the tile sees some key of this wave
       const char* qt = qtile[t & 1];
-      f32x16_t acc[2];
+      constexpr int kRB = kQTile / 32;  // 32-query row blocks per tile
+      f32x16_t acc[kRB][2];
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(col, ks * 2 + half));
+      for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
-          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[cb], 0, 0, 0);
-      }
-      // acc[cb][r]: query i0 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
-      float lr[16];
-      const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 v = lp[2 * q4 + half];  // rows 8 q4 + 4 half .. + 3
-        lr[4 * q4] = v.x;
-        lr[4 * q4 + 1] = v.y;
-        lr[4 * q4 + 2] = v.z;
-        lr[4 * q4 + 3] = v.w;
+          for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(rb * 32 + col, ks * 2 + half));
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[rb][cb], 0, 0, 0);
+        }
       }
+      // acc[rb][cb][r]: query i0 + rb*32 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
+      const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
       const bool diag = i0 < k0 + kKPerWave - 1;
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        const int j = k0 + cb * 32 + col;
-        float cs = 0.f;
-        if (diag) {
+      for (int rb = 0; rb < kRB; ++rb) {
+        float lr[16];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
-            const float p = fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
-            cs += (j <= i) ? p : 0.f;
-          }
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) cs += fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 v = lp[rb * 8 + 2 * q4 + half];  // rows rb*32 + 8 q4 + 4 half .. + 3
+          lr[4 * q4] = v.x;
+          lr[4 * q4 + 1] = v.y;
+          lr[4 * q4 + 2] = v.z;
+          lr[4 * q4 + 3] = v.w;
         }
-        csum[cb] += cs;
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+          const int j = k0 + cb * 32 + col;
+          float cs = 0.f;
+          if (diag) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int i = i0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+              const float p = fast_exp2(fmaf(acc[rb][cb][r], c2, -lr[r]));
+              cs += (j <= i) ? p : 0.f;
+            }
+          } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) cs += fast_exp2(fmaf(acc[rb][cb][r], c2, -lr[r]));
+          }
+          csum[cb] += cs;
+        }
       }
     }
     if (more && wave == 0 && lane < kQTile) ltile[(t + 1) & 1][lane] = lv;
@@ -342,14 +351,20 @@ __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restric
 
 template <int DH>
 void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
-            int Hkv, float scale, float* S, float* lse2, float* part, hipStream_t s) {
+            int Hkv, float scale, const float* lse_in, float* S, float* lse2, float* part, hipStream_t s) {
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
   const int nkb = (max_seqlen + kKBlock - 1) / kKBlock;
-  attn_lse_kernel<DH><<<dim3(size_t(nqb) * B * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
-                                                                                 nqb, c2, lse2);
+  float lse_mul = 1.f;  // row log-sum-exps in base 2 (pass 1) ...
+  if (lse_in) {         // ... or the caller's natural-log ones, converted on load
+    lse2 = const_cast<float*>(lse_in);
+    lse_mul = kLog2e;
+  } else {
+    attn_lse_kernel<DH><<<dim3(size_t(nqb) * B * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
+                                                                                   nqb, c2, lse2);
+  }
   attn_colsum_kernel<DH><<<dim3(size_t(nkb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
-                                                                                    c2, lse2, part);
+                                                                                    c2, lse2, lse_mul, part);
   attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L * Hkv, Hq, S);
 }
 
@@ -358,6 +373,40 @@ void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_
 
 using namespace estp;
 using namespace estp::detail;
+
+namespace {
+
+// Shared argument checks of the two importance entry points.
+int check_importance_args(const char* fn, const void* Q, const void* K, const int32_t* cu_seqlens, int32_t B,
+                          int32_t max_seqlen, int64_t n_tok, int32_t L, int32_t Hq, int32_t Hkv, int32_t dh,
+                          float scale, int dtype, float* S) {
+  ESTP_REQUIRE(Q && K && cu_seqlens && S, ESTP_ERR_INVALID_ARG, "%s: Q, K, cu_seqlens and S must be non-null", fn);
+  ESTP_REQUIRE(B >= 1 && max_seqlen >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1, ESTP_ERR_INVALID_ARG,
+               "%s: B, max_seqlen, L, Hq, Hkv must be >= 1", fn);
+  ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG, "%s: n_tok must be in [1, 2^31), got %lld", fn,
+               (long long)n_tok);
+  ESTP_REQUIRE(max_seqlen <= n_tok, ESTP_ERR_INVALID_ARG, "%s: max_seqlen exceeds n_tok", fn);
+  ESTP_REQUIRE(Hq % Hkv == 0, ESTP_ERR_INVALID_ARG, "%s: Hq (%d) must be a multiple of Hkv (%d)", fn, Hq, Hkv);
+  ESTP_REQUIRE(scale > 0.f && scale < INFINITY, ESTP_ERR_INVALID_ARG, "%s: scale must be finite and > 0", fn);
+  ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG, "%s: unknown dtype %d", fn, dtype);
+  ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED, "%s: only ESTP_BF16 inputs are supported", fn);
+  ESTP_REQUIRE(dh == 32 || dh == 64 || dh == 128, ESTP_ERR_UNSUPPORTED, "%s: head_dim %d unsupported (32, 64, 128)",
+               fn, dh);
+  ESTP_REQUIRE(aligned(Q, 16) && aligned(K, 16), ESTP_ERR_INVALID_ARG, "%s: Q and K must be 16-byte aligned", fn);
+  ESTP_REQUIRE(size_t(L) * Hq * n_tok < (size_t(1) << 40), ESTP_ERR_INVALID_ARG, "%s: too large", fn);
+  return ESTP_OK;
+}
+
+void launch_dh(int dh, const uint16_t* q, const uint16_t* k, const int* cu, int B, int max_seqlen, int n, int L,
+               int Hq, int Hkv, float scale, const float* lse_in, float* S, float* lse2, float* part, hipStream_t s) {
+  switch (dh) {
+    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
+    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
+    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
+  }
+}
+
+}  // namespace
 
 extern "C" size_t estp_attn_importance_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L,
                                                       int32_t Hq, int32_t Hkv, int32_t dh, int dtype) {
@@ -377,26 +426,9 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
                                     int32_t dh, float scale, int dtype, float* S, void* workspace,
                                     size_t workspace_bytes, void* stream) {
   clear_error();
-  ESTP_REQUIRE(Q && K && cu_seqlens && S, ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: Q, K, cu_seqlens and S must be non-null");
-  ESTP_REQUIRE(B >= 1 && max_seqlen >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1, ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: B, max_seqlen, L, Hq, Hkv must be >= 1");
-  ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: n_tok must be in [1, 2^31), got %lld", (long long)n_tok);
-  ESTP_REQUIRE(max_seqlen <= n_tok, ESTP_ERR_INVALID_ARG, "estp_attn_importance: max_seqlen exceeds n_tok");
-  ESTP_REQUIRE(Hq % Hkv == 0, ESTP_ERR_INVALID_ARG, "estp_attn_importance: Hq (%d) must be a multiple of Hkv (%d)",
-               Hq, Hkv);
-  ESTP_REQUIRE(scale > 0.f && scale < INFINITY, ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: scale must be finite and > 0");
-  ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: unknown dtype %d", dtype);
-  ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED,
-               "estp_attn_importance: only ESTP_BF16 inputs are supported");
-  ESTP_REQUIRE(dh == 32 || dh == 64 || dh == 128, ESTP_ERR_UNSUPPORTED,
-               "estp_attn_importance: head_dim %d unsupported (32, 64, 128)", dh);
-  ESTP_REQUIRE(aligned(Q, 16) && aligned(K, 16), ESTP_ERR_INVALID_ARG,
-               "estp_attn_importance: Q and K must be 16-byte aligned");
-  ESTP_REQUIRE(size_t(L) * Hq * n_tok < (size_t(1) << 40), ESTP_ERR_INVALID_ARG, "estp_attn_importance: too large");
+  const int st = check_importance_args("estp_attn_importance", Q, K, cu_seqlens, B, max_seqlen, n_tok, L, Hq, Hkv,
+                                       dh, scale, dtype, S);
+  if (st != ESTP_OK) return st;
   const size_t need = estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dtype);
   ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
                "estp_attn_importance: workspace of %zu bytes, %zu needed", workspace_bytes, need);
@@ -406,15 +438,45 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
   Carver c(workspace);
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const uint16_t* q = static_cast<const uint16_t*>(Q);
-  const uint16_t* k = static_cast<const uint16_t*>(K);
-  const int n = int(n_tok);
-  switch (dh) {
-    case 32: launch<32>(q, k, cu_seqlens, B, max_seqlen, n, L, Hq, Hkv, scale, S, lse2, part, s); break;
-    case 64: launch<64>(q, k, cu_seqlens, B, max_seqlen, n, L, Hq, Hkv, scale, S, lse2, part, s); break;
-    default: launch<128>(q, k, cu_seqlens, B, max_seqlen, n, L, Hq, Hkv, scale, S, lse2, part, s); break;
-  }
+  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+            int(n_tok), L, Hq, Hkv, scale, nullptr, S, lse2, part, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance");
+  return ESTP_OK;
+}
+
+extern "C" size_t estp_attn_importance_from_lse_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen,
+                                                               int32_t L, int32_t Hq, int32_t Hkv, int32_t dh,
+                                                               int dtype) {
+  (void)B;
+  (void)max_seqlen;
+  (void)Hq;
+  (void)dh;
+  (void)dtype;
+  if (n_tok < 1 || L < 1 || Hkv < 1) return 0;
+  Carver c(nullptr);
+  c.take<float>(size_t(L) * Hkv * n_tok);  // column masses [L, Hkv, n_tok]
+  return c.bytes();
+}
+
+extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const float* lse,
+                                             const int32_t* cu_seqlens, int32_t B, int32_t max_seqlen, int64_t n_tok,
+                                             int32_t L, int32_t Hq, int32_t Hkv, int32_t dh, float scale, int dtype,
+                                             float* S, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  const int st = check_importance_args("estp_attn_importance_from_lse", Q, K, cu_seqlens, B, max_seqlen, n_tok, L,
+                                       Hq, Hkv, dh, scale, dtype, S);
+  if (st != ESTP_OK) return st;
+  ESTP_REQUIRE(lse != nullptr, ESTP_ERR_INVALID_ARG, "estp_attn_importance_from_lse: lse must be non-null");
+  const size_t need = estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dtype);
+  ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
+               "estp_attn_importance_from_lse: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
+               "estp_attn_importance_from_lse: workspace must be non-null and 256-byte aligned");
+
+  Carver c(workspace);
+  float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+            int(n_tok), L, Hq, Hkv, scale, lse, S, nullptr, part, static_cast<hipStream_t>(stream));
+  ESTP_CHECK_LAUNCH("estp_attn_importance_from_lse");
   return ESTP_OK;
 }

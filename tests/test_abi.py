@@ -96,6 +96,31 @@ def test_importance_validation():
 
 
 @needs_no_gpu
+def test_importance_from_lse_validation():
+    lib = estp.load()
+    ws = lib.estp_attn_importance_from_lse_workspace_size(100, 2, 60, 1, 4, 2, 64, 0)
+    assert 0 < ws < lib.estp_attn_importance_workspace_size(100, 2, 60, 1, 4, 2, 64, 0)  # no row-LSE buffer
+    base = [FAKE, FAKE, FAKE, FAKE, 2, 60, 100, 1, 4, 2, 64, 0.125, 0, FAKE, WS, ws, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"Q": 0, "lse": 2, "B": 4, "Hq": 8, "dh": 10, "scale": 11, "dtype": 12, "wsb": 15}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_attn_importance_from_lse(*a)
+
+    assert call(Q=None) == 1
+    assert call(lse=None) == 1
+    assert call(B=0) == 1
+    assert call(Hq=5) == 1
+    assert call(scale=-1.0) == 1
+    assert call(dh=96) == 2
+    assert call(dtype=1) == 2
+    assert call(wsb=ws - 1) == 3
+    assert call(Q=UNALIGNED) == 1
+
+
+@needs_no_gpu
 def test_combine_pool_validation():
     lib = estp.load()
     ws = lib.estp_combine_pool_workspace_size(100, 2, 60, 64, 0)

@@ -152,3 +152,43 @@ def test_fullsize_long_context():
         err = np.abs(got["S"][hi - 256:hi] - tail) / tail
         print(f"long prompt {b}: last 256 keys, max rel dS = {err.max():.1e}")
         assert np.all(np.abs(got["S"][hi - 256:hi] - tail) <= 1e-3 * tail + 1e-12)
+
+
+def _torch_row_lse(Q, K, cu, scale):
+    """Row log-sum-exps [L, Hq, n_tok] from plain fp32 torch on the device, as a prefill would return them."""
+    L, n, Hq, dh = Q.shape
+    G = Hq // K.shape[2]
+    out = torch.empty(L, Hq, n, dtype=torch.float32, device=Q.device)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        N = hi - lo
+        mask = torch.ones(N, N, dtype=torch.bool, device=Q.device).tril()
+        for l in range(L):
+            q = Q[l, lo:hi].float().transpose(0, 1).contiguous()                         # [Hq, N, dh]
+            k = K[l, lo:hi].float().repeat_interleave(G, dim=1).permute(1, 2, 0).contiguous()  # [Hq, dh, N]
+            s = torch.bmm(q, k) * scale
+            s = s.masked_fill(~mask, float("-inf"))
+            out[l, :, lo:hi] = torch.logsumexp(s, dim=2)
+    return out
+
+
+def test_fullsize_llama_importance_from_prefill_lse():
+    # the one-pass entry point fed with fp32 row LSEs at the benchmark shape: exact on the
+    # last 256 keys of two prompts, and equal to the two-pass result on every token
+    w = synth.get_workload("llama")
+    inp = I.make_inputs(w, 42)
+    cu = inp["cu_seqlens"].astype(np.int64)
+    max_len = int(inp["lengths"].max())
+    Q, K, cud = dev(inp["Q"]), dev(inp["K"]), dev(inp["cu_seqlens"])
+    scale = w.dh ** -0.5
+    lse = _torch_row_lse(Q, K, cu, scale)
+    S1 = host(estp.attn_importance_from_lse(Q, K, lse, cud, max_len))
+    S2 = host(estp.attn_importance(Q, K, cud, max_len))
+    torch.cuda.synchronize()
+    assert np.all(np.abs(S1 - S2) <= 1e-3 * S2 + 1e-12)
+    for b in (0, len(cu) - 2):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        tail = oracle.attn_importance_tail(inp["Q"][:, lo:hi], inp["K"][:, lo:hi], hi - lo, 256)
+        assert np.all(np.abs(S1[hi - 256:hi] - tail) <= 1e-3 * tail + 1e-12)
+    for b in range(len(cu) - 1):
+        assert abs(S1[cu[b]:cu[b + 1]].sum() - w.L) <= 1e-3 * w.L

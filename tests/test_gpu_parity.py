@@ -122,6 +122,27 @@ def test_importance_parity(lengths, L, Hq, Hkv, dh, qs, tag):
         assert abs(S[cu[b]:cu[b + 1]].sum() - L) <= 1e-4 * L
 
 
+@pytest.mark.parametrize("lengths,L,Hq,Hkv,dh,qs,tag", IMPORTANCE_CASES, ids=[c[-1] for c in IMPORTANCE_CASES])
+def test_importance_from_lse_parity(lengths, L, Hq, Hkv, dh, qs, tag):
+    # the prefill's row normalisers (here the oracle's) replace pass 1
+    Q, K, cu = _qk(lengths, L, Hq, Hkv, dh, qs, 5)
+    lse = oracle.attn_row_lse(Q, K, cu)
+    S = host(estp.attn_importance_from_lse(dev(Q), dev(K), dev(lse.astype(np.float32)), dev(cu), max(lengths)))
+    ref = oracle.attn_importance(Q, K, cu)
+    print(f"{tag}: max rel |dS| = {(np.abs(S - ref) / ref).max():.3e}")
+    assert np.all(np.abs(S - ref) <= S_RTOL * ref + 1e-12)
+
+
+def test_importance_from_lse_uses_the_given_normalisers():
+    # normalisers off by a per-row shift scale each row: the result follows the given lse
+    Q, K, cu = _qk([70, 260, 9], 2, 4, 2, 64, 1.0, 12)
+    shifted = oracle.attn_row_lse(Q, K, cu) + np.random.default_rng(13).uniform(-0.5, 0.5, size=(2, 4, 339))
+    S = host(estp.attn_importance_from_lse(dev(Q), dev(K), dev(shifted.astype(np.float32)), dev(cu), 260))
+    ref = oracle.attn_importance_from_lse(Q, K, cu, shifted.astype(np.float32))
+    assert np.all(np.abs(S - ref) <= S_RTOL * ref + 1e-12)
+    assert not np.allclose(ref, oracle.attn_importance(Q, K, cu), rtol=1e-2)
+
+
 def test_importance_repeatable_bitwise():
     Q, K, cu = _qk([300, 45, 600], 2, 8, 2, 128, 1.0, 6)
     Qd, Kd, cud = dev(Q), dev(K), dev(cu)

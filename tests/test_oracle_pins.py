@@ -472,3 +472,48 @@ def test_length_loss():
     ce_pp = oracle.length_loss(p, p, [0.0], [0.0], 1.0)
     np.testing.assert_allclose(ce_pp, scipy.stats.entropy(p[0]), rtol=1e-14)
     assert oracle.length_loss(p, phat, [0.0], [0.0], 1.0) > ce_pp
+
+
+# ============================================================================ row normalisers (prefill LSE)
+
+def test_row_lse_bruteforce():
+    # two prompts, grouped heads: every row's log partition sum against scalar loops
+    lengths = [5, 3]
+    Q = _rng(50).standard_normal((1, 8, 4, 3)) * 1.3
+    K = _rng(51).standard_normal((1, 8, 2, 3))
+    got = oracle.attn_row_lse(Q, K, [0, 5, 8], scale=0.7)
+    ref = bruteforce.row_lse(Q[0].tolist(), K[0].tolist(), lengths, 0.7)
+    np.testing.assert_allclose(got[0], np.array(ref), rtol=1e-13, atol=1e-13)
+
+
+def test_row_lse_closed_forms():
+    # the first row of a prompt sees only itself: lse = scale q.k; zero queries: lse_i = log(i + 1)
+    Q = _rng(52).standard_normal((2, 9, 2, 4)); K = _rng(53).standard_normal((2, 9, 1, 4))
+    lse = oracle.attn_row_lse(Q, K, [0, 4, 9], scale=0.5)
+    for l in range(2):
+        for h in range(2):
+            for lo in (0, 4):
+                assert lse[l, h, lo] == pytest.approx(0.5 * Q[l, lo, h] @ K[l, lo, 0], rel=1e-14)
+    z = oracle.attn_row_lse(np.zeros((1, 6, 2, 4)), K[:1, :6], [0, 6])
+    np.testing.assert_allclose(z[0, 1], np.log(np.arange(1, 7)), rtol=1e-14)
+
+
+def test_importance_from_lse_bruteforce_and_identity():
+    lengths = [6, 2]
+    Q = _rng(54).standard_normal((1, 8, 2, 3)) * 1.2
+    K = _rng(55).standard_normal((1, 8, 1, 3))
+    cu = [0, 6, 8]
+    # with the exact normalisers the rows are softmax rows: the plain importance
+    exact = oracle.attn_row_lse(Q, K, cu, scale=0.9)
+    np.testing.assert_allclose(oracle.attn_importance_from_lse(Q, K, cu, exact, scale=0.9),
+                               oracle.attn_importance(Q, K, cu, scale=0.9), rtol=1e-13)
+    # shifted normalisers scale row i by exp(-delta_i): scalar loops agree
+    shifted = exact + _rng(56).standard_normal(exact.shape) * 0.3
+    got = oracle.attn_importance_from_lse(Q, K, cu, shifted, scale=0.9)
+    ref = bruteforce.importance_with_lse(Q[0].tolist(), K[0].tolist(), lengths, 0.9, shifted[0].tolist())
+    np.testing.assert_allclose(got, ref, rtol=1e-13)
+    # mass: sum_j S_j = (1/N) sum_i (1/Hq) sum_h exp(-delta_hi) per prompt
+    delta = shifted - exact
+    for lo, hi in ((0, 6), (6, 8)):
+        mass = np.exp(-delta[0, :, lo:hi]).mean(axis=0).sum() / (hi - lo)
+        assert got[lo:hi].sum() == pytest.approx(mass, rel=1e-13)
