@@ -86,6 +86,27 @@ def recorded_traffic(workload: str):
     return float(m.group(1)) if h.hexdigest()[:16] == m.group(2) else None
 
 
+def row_lse_torch(Q, K, cu_seqlens, scale, torch, rows: int = 1024):
+    """Row log-sum-exps [L, Hq, n_tok] of every causal attention row, plain fp32 torch on the
+    device, ``rows`` query rows at a time (stands in for what a FlashAttention-style prefill
+    returns)."""
+    L, n, Hq, _ = Q.shape
+    G = Hq // K.shape[2]
+    out = torch.empty(L, Hq, n, dtype=torch.float32, device=Q.device)
+    for b in range(len(cu_seqlens) - 1):
+        lo, hi = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+        j = torch.arange(hi - lo, device=Q.device)[None, :]
+        for l in range(L):
+            k = K[l, lo:hi].float().repeat_interleave(G, dim=1).permute(1, 2, 0).contiguous()  # [Hq, dh, N]
+            for i0 in range(0, hi - lo, rows):
+                i1 = min(hi - lo, i0 + rows)
+                q = Q[l, lo + i0:lo + i1].float().transpose(0, 1).contiguous()              # [Hq, r, dh]
+                i = torch.arange(i0, i1, device=Q.device)[:, None]
+                s = (torch.bmm(q, k) * scale).masked_fill(j > i, float("-inf"))
+                out[l, :, lo + i0:lo + i1] = torch.logsumexp(s, dim=2)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -184,6 +205,24 @@ def main() -> int:
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step "
         f"(entropy {ent_ms:.3f}, importance {imp_ms:.3f}, combine+pool {pool_ms:.3f}, head {pred_ms:.3f} ms)")
 
+    # The one-pass importance call fed with a prefill's row log-sum-exps (here formed with plain
+    # fp32 torch, untimed); timed on its own, outside the step.
+    lse = row_lse_torch(Q, K, inp["cu_seqlens"], w.dh ** -0.5, torch)
+    ws_lse = torch.empty(estp.load().estp_attn_importance_from_lse_workspace_size(n_tok, B, max_len, w.L, w.Hq, w.Hkv,
+                                                                                 w.dh, 0),
+                         dtype=torch.uint8, device=X.device)
+    S_lse = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+    estp.attn_importance_from_lse(Q, K, lse, cu, max_len, S=S_lse, workspace=ws_lse, stream=stream)
+    lse_evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for k in range(5):
+        lse_evs[k].record(stream)
+        estp.attn_importance_from_lse(Q, K, lse, cu, max_len, S=S_lse, workspace=ws_lse, stream=stream)
+    lse_evs[5].record(stream)
+    torch.cuda.synchronize()
+    lse_ms = float(np.mean([lse_evs[k].elapsed_time(lse_evs[k + 1]) for k in range(5)]))
+    del lse, ws_lse, S_lse
+    log(f"importance from prefill LSE: {lse_ms:.3f} ms (two-pass call {imp_ms:.3f} ms)")
+
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
     pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
@@ -222,6 +261,9 @@ def main() -> int:
                        "predict": pred_ms},
         "importance": {"alg_flop": imp_flop_alg, "alg_tflops": imp_flop_alg / (imp_ms * 1e-3) / 1e12,
                        "executed_tflops": 2 * imp_flop_alg / (imp_ms * 1e-3) / 1e12},
+        "importance_from_prefill_lse": {"ms": lse_ms, "vs_two_pass": lse_ms / imp_ms,
+                                        "note": "estp_attn_importance_from_lse with given row LSEs; not part of "
+                                                "the timed step"},
         "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
                     "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
                     "note": "whole combine_pool call (weights + pooling + chunk reduction), warm after importance"},
