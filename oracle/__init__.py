@@ -17,6 +17,8 @@ exactly to float64 and evaluates the paper's definitions:
 * ``pool``               - Eq. 5 (Section 4.2)
 * ``predict``            - the MLP length head with Eq. 7 (Section 4.3)
 * ``soft_labels``, ``length_loss`` - Eq. 6 and Eq. 8 (Section 4.3)
+* ``length_bin``, ``head_loss_and_grads``, ``adamw_step``, ``head_train_step`` - one
+  training step of the K-bin head: Eq. 8 loss, its gradients, AdamW (Section 5.1)
 
 ``oracle.bruteforce`` re-derives the same quantities with pure-Python loops
 for tiny shapes; the tests pin this module against it, against closed forms
@@ -34,5 +36,9 @@ from .estp_oracle import (  # noqa: F401
     predict,
     soft_labels,
     length_loss,
+    length_bin,
+    head_loss_and_grads,
+    adamw_step,
+    head_train_step,
     run_path,
 )

@@ -335,6 +335,90 @@ def length_loss(p, phat, y, yhat, lambda3: float) -> float:
     return float(lambda3 * ce + (1.0 - lambda3) * mse)
 
 
+# ----------------------------------------------------------------------------- training the head
+
+def length_bin(y, edges) -> np.ndarray:
+    """Index i of the bin [edges[i], edges[i+1]) holding each length; below the first
+    edge -> 0, at or above the last -> K-1 (K = len(edges) - 1).  The ground-truth bin
+    of Eq. 6."""
+    e = np.asarray(edges, dtype=np.float64)
+    K = len(e) - 1
+    i = np.searchsorted(e[1:K], np.asarray(y, dtype=np.float64), side="right")
+    return np.clip(i, 0, K - 1)
+
+
+def _act_grad(a: np.ndarray, act: str) -> np.ndarray:
+    """d act(a) / d a."""
+    if act == "relu":
+        return (a > 0.0).astype(np.float64)
+    if act == "gelu_tanh":
+        k = math.sqrt(2.0 / math.pi)
+        u = k * (a + 0.044715 * a ** 3)
+        t = np.tanh(u)
+        return 0.5 * (1.0 + t) + 0.5 * a * (1.0 - t * t) * k * (1.0 + 3 * 0.044715 * a * a)
+    raise ValueError(act)
+
+
+def head_loss_and_grads(pooled, y, edges, centres, W1, b1, W2, b2, lambda3: float, act: str = "relu"):
+    """Eq. 8 loss of the K-bin head (Section 4.3) on one batch and its gradients.
+
+    Forward: a = act(W1 h + b1), o = W2 a + b2, p-hat = softmax(o), y-hat = sum_k p-hat_k c_k
+    (Eq. 7); target p = Eq. 6 soft labels around the true bin; loss = lambda3 CE(p, p-hat)
+    + (1 - lambda3) (y - y-hat)^2, both averaged over the batch.  Gradients by the chain rule,
+    written out layer by layer.  Returns ``(loss, {"W1", "b1", "W2", "b2"})``.
+    """
+    h = np.asarray(pooled, dtype=np.float64)
+    y = np.asarray(y, dtype=np.float64)
+    c = np.asarray(centres, dtype=np.float64)
+    W1, b1, W2, b2 = (np.asarray(t, dtype=np.float64) for t in (W1, b1, W2, b2))
+    B, K = h.shape[0], W2.shape[0]
+    z = h @ W1.T + b1
+    a = _act(z, act)
+    o = a @ W2.T + b2
+    lse = o.max(axis=1, keepdims=True) + np.log(np.exp(o - o.max(axis=1, keepdims=True)).sum(axis=1, keepdims=True))
+    phat = np.exp(o - lse)
+    yhat = phat @ c
+    p = np.stack([soft_labels(int(i), K) for i in length_bin(y, edges)])
+    loss = length_loss(p, phat, y, yhat, lambda3)
+    # dL/do: cross-entropy of a softmax, and the squared error through the expectation
+    d_ce = phat - p
+    d_mse = (-2.0 * (y - yhat))[:, None] * phat * (c[None, :] - yhat[:, None])
+    do = (lambda3 * d_ce + (1.0 - lambda3) * d_mse) / B
+    g = {"W2": do.T @ a, "b2": do.sum(axis=0)}
+    dz = (do @ W2) * _act_grad(z, act)
+    g["W1"] = dz.T @ h
+    g["b1"] = dz.sum(axis=0)
+    return loss, g
+
+
+def adamw_step(theta, grad, m, v, t: int, lr: float, beta1: float, beta2: float, eps: float,
+               weight_decay: float):
+    """One AdamW step (decoupled weight decay), as the paper's optimiser (Section 5.1):
+    theta <- theta (1 - lr wd); m, v <- moment updates; theta <- theta - lr m_hat / (sqrt(v_hat) + eps)
+    with bias-corrected m_hat = m / (1 - beta1^t), v_hat = v / (1 - beta2^t).
+    Returns ``(theta, m, v)`` (new arrays)."""
+    theta = np.asarray(theta, dtype=np.float64) * (1.0 - lr * weight_decay)
+    m = beta1 * np.asarray(m, dtype=np.float64) + (1.0 - beta1) * grad
+    v = beta2 * np.asarray(v, dtype=np.float64) + (1.0 - beta2) * grad * grad
+    mhat = m / (1.0 - beta1 ** t)
+    vhat = v / (1.0 - beta2 ** t)
+    return theta - lr * mhat / (np.sqrt(vhat) + eps), m, v
+
+
+def head_train_step(pooled, y, edges, centres, params, m, v, t: int, lambda3: float, lr: float,
+                    beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8, weight_decay: float = 0.01,
+                    act: str = "relu"):
+    """One training step of the length head: Eq. 8 loss and gradients at ``params``
+    (dict W1, b1, W2, b2), then AdamW on every tensor.  ``m``, ``v`` are dicts of the same
+    shapes.  Returns ``(loss, grads, params, m, v)`` with the updated dicts."""
+    loss, g = head_loss_and_grads(pooled, y, edges, centres, params["W1"], params["b1"], params["W2"],
+                                  params["b2"], lambda3, act)
+    P, M, Vv = {}, {}, {}
+    for k in ("W1", "b1", "W2", "b2"):
+        P[k], M[k], Vv[k] = adamw_step(params[k], g[k], m[k], v[k], t, lr, beta1, beta2, eps, weight_decay)
+    return loss, g, P, M, Vv
+
+
 # ----------------------------------------------------------------------------- whole path
 
 def run_path(X, W, Q, K, cu_seqlens, lambda1: float, lambda2: float, alpha: float = 1.0,

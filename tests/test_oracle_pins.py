@@ -517,3 +517,86 @@ def test_importance_from_lse_bruteforce_and_identity():
     for lo, hi in ((0, 6), (6, 8)):
         mass = np.exp(-delta[0, :, lo:hi]).mean(axis=0).sum() / (hi - lo)
         assert got[lo:hi].sum() == pytest.approx(mass, rel=1e-13)
+
+
+# ============================================================================ training the length head
+
+def _head_problem(seed, B=5, d=6, Hd=4, K=5, act="relu"):
+    g = _rng(seed)
+    h = g.standard_normal((B, d))
+    params = {"W1": g.standard_normal((Hd, d)) * 0.7, "b1": g.standard_normal(Hd) * 0.3,
+              "W2": g.standard_normal((K, Hd)) * 0.7, "b2": g.standard_normal(K) * 0.3}
+    edges = np.linspace(0.0, 50.0 * K, K + 1)
+    centres = 0.5 * (edges[1:] + edges[:-1])
+    y = g.uniform(-10.0, 50.0 * K + 10.0, size=B)
+    return h, y, edges, centres, params
+
+
+@pytest.mark.parametrize("act", ["relu", "gelu_tanh"])
+def test_head_gradients_match_finite_differences(act):
+    # central differences of the Eq. 8 loss pin every analytic gradient entry
+    h, y, edges, centres, P = _head_problem(60, act=act)
+    lam = 0.3
+    # keep ReLU pre-activations away from the kink so the difference quotient is smooth
+    z = h @ P["W1"].T + P["b1"]
+    assert np.abs(z).min() > 1e-3
+    loss, g = oracle.head_loss_and_grads(h, y, edges, centres, P["W1"], P["b1"], P["W2"], P["b2"], lam, act)
+    eps = 1e-6
+    for name in ("W1", "b1", "W2", "b2"):
+        fd = np.zeros_like(P[name])
+        for idx in np.ndindex(P[name].shape):
+            Pp = {k: v.copy() for k, v in P.items()}
+            Pm = {k: v.copy() for k, v in P.items()}
+            Pp[name][idx] += eps
+            Pm[name][idx] -= eps
+            lp, _ = oracle.head_loss_and_grads(h, y, edges, centres, Pp["W1"], Pp["b1"], Pp["W2"], Pp["b2"], lam, act)
+            lm, _ = oracle.head_loss_and_grads(h, y, edges, centres, Pm["W1"], Pm["b1"], Pm["W2"], Pm["b2"], lam, act)
+            fd[idx] = (lp - lm) / (2 * eps)
+        np.testing.assert_allclose(g[name], fd, rtol=1e-5, atol=1e-7 * max(1.0, abs(loss)))
+
+
+def test_head_loss_closed_form():
+    # W2 = 0, b2 = 0: p-hat uniform over 2 bins, CE = log 2 whatever the soft labels, y-hat the mean centre
+    h = np.ones((3, 4))
+    W1 = np.ones((2, 4)); b1 = np.zeros(2)
+    y = np.array([3.0, 15.0, 40.0])
+    edges = np.array([0.0, 10.0, 20.0]); centres = np.array([5.0, 15.0])
+    lam = 0.25
+    loss, _ = oracle.head_loss_and_grads(h, y, edges, centres, W1, b1, np.zeros((2, 2)), np.zeros(2), lam)
+    assert loss == pytest.approx(lam * math.log(2.0) + (1 - lam) * np.mean((y - 10.0) ** 2), rel=1e-14)
+
+
+def test_length_bin_edges():
+    edges = [0.0, 10.0, 20.0, 30.0]
+    assert list(oracle.length_bin([-5.0, 0.0, 9.99, 10.0, 19.0, 20.0, 29.9, 30.0, 100.0], edges)) == \
+        [0, 0, 0, 1, 1, 2, 2, 2, 2]
+
+
+def test_adamw_closed_forms():
+    # first step: m_hat = g, v_hat = g^2, so each coordinate moves by lr g / (|g| + eps) after decay
+    th = np.array([1.0, -2.0, 0.5]); g = np.array([0.3, -4.0, 0.0])
+    new, m, v = oracle.adamw_step(th, g, np.zeros(3), np.zeros(3), 1, 0.1, 0.9, 0.999, 1e-8, 0.01)
+    np.testing.assert_allclose(new, th * (1 - 0.001) - 0.1 * g / (np.abs(g) + 1e-8), rtol=1e-15)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-15)
+    np.testing.assert_allclose(v, 0.001 * g * g, rtol=1e-15)
+    # second step on a scalar, by hand
+    m2 = 0.9 * 0.03 + 0.1 * 0.5
+    v2 = 0.999 * 0.001 * 0.09 + 0.001 * 0.25
+    exp = (1.0 * (1 - 0.001) - 0.1 * 0.3 / (0.3 + 1e-8)) * (1 - 0.001) \
+        - 0.1 * (m2 / (1 - 0.81)) / (math.sqrt(v2 / (1 - 0.999 ** 2)) + 1e-8)
+    n1, m1, v1 = oracle.adamw_step(np.array([1.0]), np.array([0.3]), np.zeros(1), np.zeros(1), 1, 0.1, 0.9, 0.999,
+                                   1e-8, 0.01)
+    n2, _, _ = oracle.adamw_step(n1, np.array([0.5]), m1, v1, 2, 0.1, 0.9, 0.999, 1e-8, 0.01)
+    assert n2[0] == pytest.approx(exp, rel=1e-14)
+
+
+def test_head_training_reduces_loss():
+    # a few AdamW steps on a fixed batch lower the Eq. 8 loss
+    h, y, edges, centres, P = _head_problem(61, B=16, d=8, Hd=16, K=6)
+    M = {k: np.zeros_like(v) for k, v in P.items()}
+    Vv = {k: np.zeros_like(v) for k, v in P.items()}
+    losses = []
+    for t in range(1, 41):
+        loss, _, P, M, Vv = oracle.head_train_step(h, y, edges, centres, P, M, Vv, t, 0.5, 3e-2)
+        losses.append(loss)
+    assert losses[-1] < 0.5 * losses[0]
