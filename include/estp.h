@@ -197,6 +197,40 @@ ESTP_API int estp_predict(const float* pooled, int32_t B, int32_t d, const float
                  int act, const float* W2, const float* b2, int32_t K, const float* centres, float* yhat,
                  int32_t* bin, int32_t* order, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * One training step of the K-bin length head (Eq. 6, Eq. 7, Eq. 8,
+ * Section 4.3; AdamW, Section 5.1).
+ *
+ *   z = W1 h + b1, a = act(z), o = W2 a + b2, p-hat = softmax(o),
+ *   y-hat = sum_k p-hat_k c_k                                       (Eq. 7)
+ *   i = bin of the true length y: [edges[i], edges[i+1]); below edges[0] -> 0,
+ *       at or above edges[K] -> K-1
+ *   p_j = exp(-|j - i|) / sum_k exp(-|k - i|)                        (Eq. 6)
+ *   loss = lambda3 * mean_b CE(p, p-hat) + (1 - lambda3) * mean_b (y - y-hat)^2   (Eq. 8)
+ *
+ * then the gradient of the loss at the current parameters and one AdamW
+ * update of every parameter (PyTorch's form: decoupled decay
+ * theta *= 1 - lr*weight_decay, moments m, v, bias corrections 1 - beta^step).
+ *
+ *   pooled [B, d]   float32 features (the pooled vectors), 16-byte aligned
+ *   y [B]           float32 true lengths
+ *   edges [K+1]     float32 ascending bin edges;  centres [K] float32 bin centres
+ *   theta           float32 parameters, updated in place, flat layout
+ *                   [W1 (hidden x d) | b1 (hidden) | W2 (K x hidden) | b2 (K)];
+ *                   pointers into it serve estp_predict directly
+ *   m, v            float32 AdamW moments, same layout, updated in place
+ *                   (zero before step 1)
+ *   step            1-based step count (bias corrections)
+ *   loss            float32 device scalar: the batch loss before the update, or NULL
+ * Requires 2 <= K <= 1024, d % 4 == 0, lambda3 in [0, 1], betas in [0, 1),
+ * eps > 0; theta, m, v 16-byte aligned.  Batch sums run in a fixed order.
+ * ------------------------------------------------------------------------ */
+ESTP_API size_t estp_head_train_step_workspace_size(int32_t B, int32_t d, int32_t hidden, int32_t K);
+ESTP_API int estp_head_train_step(const float* pooled, const float* y, int32_t B, int32_t d, int32_t hidden, int32_t K,
+                         int act, const float* edges, const float* centres, float* theta, float* m, float* v,
+                         int32_t step, float lambda3, float lr, float beta1, float beta2, float eps,
+                         float weight_decay, float* loss, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

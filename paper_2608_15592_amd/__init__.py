@@ -7,6 +7,7 @@ Python face of libestp.so: the four calls of the ESTP path (arXiv 2608.15592)
 * ``attn_importance_from_lse`` - Eq. 1 from a prefill's per-row log-sum-exps (one pass)
 * ``combine_pool``    - Eq. 3-5, temperature softmax of the fused score and weighted pooling
 * ``predict``         - length head (Section 4.3, Eq. 7) and shortest-job-first order
+* ``head_train_step`` - one Eq. 6-8 / AdamW training step of the K-bin head
 
 plus ``run_path`` chaining them.  All computation runs in the library's HIP
 kernels; torch only supplies device memory and the stream.
@@ -20,6 +21,8 @@ from ._lib import (  # noqa: F401
     combine_pool,
     load,
     predict,
+    head_param_views,
+    head_train_step,
     token_entropy,
     token_entropy_workspace_size,
 )

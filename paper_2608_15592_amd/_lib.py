@@ -30,6 +30,7 @@ EXPORTS = (
     "estp_attn_importance_from_lse_workspace_size", "estp_attn_importance_from_lse",
     "estp_combine_pool_workspace_size", "estp_combine_pool",
     "estp_predict_workspace_size", "estp_predict",
+    "estp_head_train_step_workspace_size", "estp_head_train_step",
 )
 
 
@@ -86,6 +87,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_predict_workspace_size.argtypes = [_I32, _I32, _I32, _I32]
     lib.estp_predict.restype = _INT
     lib.estp_predict.argtypes = [_P, _I32, _I32, _P, _P, _I32, _INT, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.estp_head_train_step_workspace_size.restype = _SZ
+    lib.estp_head_train_step_workspace_size.argtypes = [_I32, _I32, _I32, _I32]
+    lib.estp_head_train_step.restype = _INT
+    lib.estp_head_train_step.argtypes = [_P, _P, _I32, _I32, _I32, _I32, _INT, _P, _P, _P, _P, _P, _I32, _F, _F, _F,
+                                         _F, _F, _F, _P, _P, _SZ, _P]
     _lib = lib
     return lib
 
@@ -284,3 +290,43 @@ def predict(pooled: torch.Tensor, W1: torch.Tensor, b1: Optional[torch.Tensor], 
                             _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb,
                             _stream(stream)), "estp_predict")
     return yhat, bins, order
+
+
+def head_param_views(theta: torch.Tensor, d: int, hidden: int, K: int):
+    """(W1, b1, W2, b2) views into a flat parameter vector laid out as estp_head_train_step expects."""
+    n1 = hidden * d
+    W1 = theta[:n1].view(hidden, d)
+    b1 = theta[n1:n1 + hidden]
+    W2 = theta[n1 + hidden:n1 + hidden + K * hidden].view(K, hidden)
+    b2 = theta[n1 + hidden + K * hidden:n1 + hidden + K * hidden + K]
+    return W1, b1, W2, b2
+
+
+def head_train_step(pooled: torch.Tensor, y: torch.Tensor, edges: torch.Tensor, centres: torch.Tensor,
+                    theta: torch.Tensor, m: torch.Tensor, v: torch.Tensor, hidden: int, step: int,
+                    lambda3: float, lr: float, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+                    weight_decay: float = 0.01, act: str = "relu", loss: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """One Eq. 8 / AdamW step of the K-bin length head; updates ``theta``, ``m``, ``v`` in place and
+    returns the batch loss (a 1-element device tensor) computed before the update."""
+    lib = load()
+    _need(pooled, "pooled", dtype=torch.float32, ndim=2)
+    dev_ = pooled.device
+    for t, n in ((y, "y"), (edges, "edges"), (centres, "centres"), (theta, "theta"), (m, "m"), (v, "v")):
+        _need(t, n, device=dev_, dtype=torch.float32, ndim=1)
+    B, d = pooled.shape
+    K = centres.numel()
+    if edges.numel() != K + 1 or y.numel() != B:
+        raise ValueError("edges must hold K+1 values and y B values")
+    n = hidden * d + hidden + K * hidden + K
+    if theta.numel() != n or m.numel() != n or v.numel() != n:
+        raise ValueError(f"theta, m, v must hold {n} values")
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=dev_)
+    workspace, wsb = _workspace(lib.estp_head_train_step_workspace_size(B, d, hidden, K), dev_, workspace)
+    _check(lib.estp_head_train_step(_ptr(pooled), _ptr(y), B, d, hidden, K, ACTS[act], _ptr(edges), _ptr(centres),
+                                    _ptr(theta), _ptr(m), _ptr(v), int(step), float(lambda3), float(lr),
+                                    float(beta1), float(beta2), float(eps), float(weight_decay), _ptr(loss),
+                                    _ptr(workspace), wsb, _stream(stream)),
+           "estp_head_train_step")
+    return loss

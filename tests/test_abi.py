@@ -180,3 +180,33 @@ def _load_fresh(path):
         return _lib.load(path)
     finally:
         _lib._lib = saved
+
+
+@needs_no_gpu
+def test_head_train_step_validation():
+    lib = estp.load()
+    ws = lib.estp_head_train_step_workspace_size(8, 64, 32, 6)
+    assert ws > 0
+    base = [FAKE, FAKE, 8, 64, 32, 6, 0, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0.5, 1e-3, 0.9, 0.999, 1e-8, 0.01, None, WS,
+            ws, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"pooled": 0, "B": 2, "d": 3, "K": 5, "act": 6, "theta": 9, "step": 12, "lambda3": 13, "lr": 14,
+               "beta1": 15, "eps": 17, "wsb": 21}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_head_train_step(*a)
+
+    assert call(pooled=None) == 1
+    assert call(B=0) == 1
+    assert call(K=1) == 1                 # Eq. 8 needs bins
+    assert call(d=66) == 1                # d % 4
+    assert call(act=5) == 1
+    assert call(step=0) == 1
+    assert call(lambda3=1.5) == 1
+    assert call(lr=-1.0) == 1
+    assert call(beta1=1.0) == 1
+    assert call(eps=0.0) == 1
+    assert call(theta=UNALIGNED) == 1
+    assert call(wsb=ws - 1) == 3
