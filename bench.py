@@ -12,6 +12,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -223,6 +224,30 @@ def main() -> int:
     del lse, ws_lse, S_lse
     log(f"importance from prefill LSE: {lse_ms:.3f} ms (two-pass call {imp_ms:.3f} ms)")
 
+    # One training step of a 16-bin head on the step's pooled vectors (Eq. 6-8, AdamW), timed on
+    # its own: W1 [1024, d] dominates, read and written with its two moments.
+    K_tr, Hd_tr = 16, 1024
+    g_tr = torch.Generator(device="cpu").manual_seed(args.seed)
+    n_par = Hd_tr * w.d + Hd_tr + K_tr * Hd_tr + K_tr
+    theta = (torch.randn(n_par, generator=g_tr) * 0.02).to(X.device)
+    m_tr, v_tr = torch.zeros_like(theta), torch.zeros_like(theta)
+    edges = torch.cat([torch.zeros(1), torch.logspace(6, 14, K_tr, base=2.0)]).to(X.device)
+    centres = 0.5 * (edges[1:] + edges[:-1])
+    y_tr = torch.exp(torch.empty(B).uniform_(math.log(16.0), math.log(16384.0), generator=g_tr)).to(X.device)
+    pooled_tr = bufs["pooled"]
+    estp.head_train_step(pooled_tr, y_tr, edges, centres, theta, m_tr, v_tr, Hd_tr, 1, 0.5, 1e-4, stream=stream)
+    tr_evs = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+    for k in range(10):
+        tr_evs[k].record(stream)
+        estp.head_train_step(pooled_tr, y_tr, edges, centres, theta, m_tr, v_tr, Hd_tr, k + 2, 0.5, 1e-4,
+                             stream=stream)
+    tr_evs[10].record(stream)
+    torch.cuda.synchronize()
+    tr_ms = float(np.mean([tr_evs[k].elapsed_time(tr_evs[k + 1]) for k in range(10)]))
+    tr_bytes = 6 * 4 * n_par + 4 * B * w.d
+    del theta, m_tr, v_tr
+    log(f"head training step (B={B}, {w.d}->{Hd_tr}->{K_tr}): {tr_ms:.3f} ms")
+
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
     pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
@@ -264,6 +289,9 @@ def main() -> int:
         "importance_from_prefill_lse": {"ms": lse_ms, "vs_two_pass": lse_ms / imp_ms,
                                         "note": "estp_attn_importance_from_lse with given row LSEs; not part of "
                                                 "the timed step"},
+        "head_train_step": {"ms": tr_ms, "head": f"{w.d}->{Hd_tr}->{K_tr}", "batch": B, "param_bytes_rw": tr_bytes,
+                            "achieved_GBps": tr_bytes / (tr_ms * 1e-3) / 1e9,
+                            "note": "estp_head_train_step (Eq. 8 loss, backward, AdamW); not part of the timed step"},
         "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
                     "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
                     "note": "whole combine_pool call (weights + pooling + chunk reduction), warm after importance"},
