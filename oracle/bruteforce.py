@@ -34,8 +34,9 @@ def entropy_rows(X, W):
     return out
 
 
-def importance(Q, K, lengths, scale):
-    """S for one layer: Q[t][h][k], K[t][g][k] nested lists, prompts given by ``lengths`` (Eq. 1)."""
+def importance(Q, K, lengths, scale, exclude_self=False):
+    """S for one layer: Q[t][h][k], K[t][g][k] nested lists, prompts given by ``lengths`` (Eq. 1);
+    ``exclude_self`` leaves the diagonal out of the column sums."""
     Hq = len(Q[0])
     Hkv = len(K[0])
     G = Hq // Hkv
@@ -57,7 +58,7 @@ def importance(Q, K, lengths, scale):
                 for j in range(i + 1):
                     Aavg[i][j] += math.exp(s[j] - smax) / den / Hq
         for j in range(N):
-            S.append(math.fsum(Aavg[i][j] for i in range(N)) / N)
+            S.append(math.fsum(Aavg[i][j] for i in range(N) if not (exclude_self and i == j)) / N)
         start += N
     return S
 

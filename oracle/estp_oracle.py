@@ -81,14 +81,18 @@ def _causal_softmax_rows(s: np.ndarray, i0: int) -> np.ndarray:
     return p / p.sum(axis=1, keepdims=True)
 
 
-def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: int = 2048) -> np.ndarray:
+def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: int = 2048,
+                    exclude_self: bool = False, layer_weights=None) -> np.ndarray:
     """S_j = (1/N) sum_i A_ij with A the head-averaged causal attention (Eq. 1).
 
     ``Q`` [L, n_tok, Hq, dh] and ``K`` [L, n_tok, Hkv, dh] are post-RoPE
     queries and keys of L layers, packed over prompts by ``cu_seqlens``
-    [B+1]; the result [n_tok] sums the per-layer importance.  Query rows are
-    taken ``row_chunk`` at a time (the column sum over i is split into
-    consecutive ranges); each attention row is complete.
+    [B+1]; the result [n_tok] sums the per-layer importance, each layer
+    weighted by ``layer_weights[l]`` when given.  Query rows are taken
+    ``row_chunk`` at a time (the column sum over i is split into consecutive
+    ranges); each attention row is complete.  ``exclude_self`` drops the
+    diagonal term A_jj from the column sum (the rows themselves still include
+    it): the variant reading of the paper's note on self-similarity.
     """
     Qd = widen(Q)
     Kd = widen(K)
@@ -116,8 +120,11 @@ def attn_importance(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: 
                 for i0 in range(0, N, row_chunk):
                     s = scale * (q[i0:i0 + row_chunk] @ k.T)
                     A = _causal_softmax_rows(s, i0)
+                    if exclude_self:
+                        r = np.arange(A.shape[0])
+                        A[r, i0 + r] = 0.0
                     colsum += A.sum(axis=0) / Hq
-            S[lo:hi] += colsum / N
+            S[lo:hi] += (1.0 if layer_weights is None else float(layer_weights[l])) * colsum / N
     return S
 
 
@@ -158,12 +165,12 @@ def attn_row_lse(Q, K, cu_seqlens, scale: Optional[float] = None, row_chunk: int
 
 
 def attn_importance_from_lse(Q, K, cu_seqlens, lse, scale: Optional[float] = None,
-                             row_chunk: int = 2048) -> np.ndarray:
+                             row_chunk: int = 2048, exclude_self: bool = False, layer_weights=None) -> np.ndarray:
     """S_j of Eq. 1 with row i of every head normalised by the given ``lse`` [L, Hq, n_tok]:
     A_ij = exp(scale q_i . k_j - lse_i) for j <= i, then averaged over heads,
     summed over i and divided by N as in ``attn_importance``.  With
     ``lse = attn_row_lse(...)`` the rows are the causal softmax rows and the
-    result is ``attn_importance``.
+    result is ``attn_importance``.  ``exclude_self`` and ``layer_weights`` as there.
     """
     Qd = widen(Q)
     Kd = widen(K)
@@ -191,9 +198,10 @@ def attn_importance_from_lse(Q, K, cu_seqlens, lse, scale: Optional[float] = Non
                 for i0 in range(0, N, row_chunk):
                     s = scale * (q[i0:i0 + row_chunk] @ k.T)
                     i = np.arange(i0, i0 + s.shape[0])[:, None]
-                    A = np.where(j <= i, np.exp(s - lse[l, h, lo + i0:lo + i0 + s.shape[0]][:, None]), 0.0)
+                    keep = (j < i) if exclude_self else (j <= i)
+                    A = np.where(keep, np.exp(s - lse[l, h, lo + i0:lo + i0 + s.shape[0]][:, None]), 0.0)
                     colsum += A.sum(axis=0) / Hq
-            S[lo:hi] += colsum / N
+            S[lo:hi] += (1.0 if layer_weights is None else float(layer_weights[l])) * colsum / N
     return S
 
 

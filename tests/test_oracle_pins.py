@@ -600,3 +600,32 @@ def test_head_training_reduces_loss():
         loss, _, P, M, Vv = oracle.head_train_step(h, y, edges, centres, P, M, Vv, t, 0.5, 3e-2)
         losses.append(loss)
     assert losses[-1] < 0.5 * losses[0]
+
+
+# ============================================================================ importance variants
+
+def test_importance_exclude_self_bruteforce_and_diagonal():
+    lengths = [7, 4]
+    Q = _rng(70).standard_normal((1, 11, 4, 3)) * 1.4
+    K = _rng(71).standard_normal((1, 11, 2, 3))
+    cu = [0, 7, 11]
+    ex = oracle.attn_importance(Q, K, cu, scale=0.8, exclude_self=True)
+    ref = bruteforce.importance(Q[0].tolist(), K[0].tolist(), lengths, 0.8, exclude_self=True)
+    np.testing.assert_allclose(ex, ref, rtol=1e-13)
+    # the excluded mass is the head-averaged diagonal: the first token of a prompt loses 1/N exactly
+    inc = oracle.attn_importance(Q, K, cu, scale=0.8)
+    assert inc[0] - ex[0] == pytest.approx(1.0 / 7, rel=1e-13)
+    assert inc[7] - ex[7] == pytest.approx(1.0 / 4, rel=1e-13)
+    # and through given row normalisers the same
+    lse = oracle.attn_row_lse(Q, K, cu, scale=0.8)
+    np.testing.assert_allclose(oracle.attn_importance_from_lse(Q, K, cu, lse, scale=0.8, exclude_self=True), ex,
+                               rtol=1e-13)
+
+
+def test_importance_layer_weights_linear():
+    Q = _rng(72).standard_normal((3, 9, 2, 4)); K = _rng(73).standard_normal((3, 9, 1, 4))
+    cu = [0, 5, 9]
+    w = [0.5, -1.0, 2.0]
+    per_layer = [oracle.attn_importance(Q[l:l + 1], K[l:l + 1], cu) for l in range(3)]
+    np.testing.assert_allclose(oracle.attn_importance(Q, K, cu, layer_weights=w),
+                               sum(wl * s for wl, s in zip(w, per_layer)), rtol=1e-13)
