@@ -154,6 +154,34 @@ ESTP_API int estp_attn_importance_from_lse(const void* Q, const void* K, const f
                                   size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Attention importance, variants (Eq. 1, Section 4.1).
+ *
+ *   S[j] = sum_l w_l (1/N_b) sum_{i in I(j)} (1/Hq) sum_h A^{l,h}_{ij}
+ *
+ * with I(j) = {i >= j} (the diagonal included, as estp_attn_importance) or,
+ * with ESTP_IMPORTANCE_EXCLUDE_SELF in `flags`, I(j) = {i > j}: each token's
+ * attention to itself is left out of the column sums (the rows A^{l,h}_{i.}
+ * are still the causal softmax over j <= i).  This is the other reading of
+ * the paper's note on self-similarity.
+ *
+ *   lse            NULL: the row log-sum-exps are computed (two passes, as
+ *                  estp_attn_importance); else the caller's natural-log
+ *                  [L, Hq, n_tok] row normalisers (one pass, as
+ *                  estp_attn_importance_from_lse)
+ *   layer_weights  host float32 [L], finite, at most 64 layers; NULL = all 1
+ *   flags          0 or ESTP_IMPORTANCE_EXCLUDE_SELF
+ * Workspace: estp_attn_importance_ex_workspace_size(..., with_lse = lse != NULL).
+ * Other arguments and requirements are those of estp_attn_importance.
+ * ------------------------------------------------------------------------ */
+#define ESTP_IMPORTANCE_EXCLUDE_SELF 1
+ESTP_API size_t estp_attn_importance_ex_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L, int32_t Hq,
+                                              int32_t Hkv, int32_t dh, int dtype, int with_lse);
+ESTP_API int estp_attn_importance_ex(const void* Q, const void* K, const float* lse, const int32_t* cu_seqlens, int32_t B,
+                            int32_t max_seqlen, int64_t n_tok, int32_t L, int32_t Hq, int32_t Hkv, int32_t dh,
+                            float scale, const float* layer_weights, int flags, int dtype, float* S, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Fusion and pooling (Eq. 3, Eq. 4, Eq. 5, Section 4.2).
  *
  *   T_i = lambda1 S_i + lambda2 H_i              (after `norm`, per prompt)

@@ -20,6 +20,7 @@ LIB_PATH = os.environ.get("ESTP_LIBRARY") or os.path.join(_HERE, "libestp.so")
 
 ESTP_OK, ESTP_ERR_INVALID_ARG, ESTP_ERR_UNSUPPORTED, ESTP_ERR_WORKSPACE, ESTP_ERR_HIP = range(5)
 ESTP_BF16, ESTP_F32 = 0, 1
+ESTP_IMPORTANCE_EXCLUDE_SELF = 1
 NORMS = {"none": 0, "zscore": 1}
 ACTS = {"relu": 0, "gelu_tanh": 1}
 
@@ -28,6 +29,7 @@ EXPORTS = (
     "estp_token_entropy_workspace_size", "estp_token_entropy",
     "estp_attn_importance_workspace_size", "estp_attn_importance",
     "estp_attn_importance_from_lse_workspace_size", "estp_attn_importance_from_lse",
+    "estp_attn_importance_ex_workspace_size", "estp_attn_importance_ex",
     "estp_combine_pool_workspace_size", "estp_combine_pool",
     "estp_predict_workspace_size", "estp_predict",
     "estp_head_train_step_workspace_size", "estp_head_train_step",
@@ -78,6 +80,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_attn_importance_from_lse.restype = _INT
     lib.estp_attn_importance_from_lse.argtypes = [_P, _P, _P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _I32, _F,
                                                   _INT, _P, _P, _SZ, _P]
+    lib.estp_attn_importance_ex_workspace_size.restype = _SZ
+    lib.estp_attn_importance_ex_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _I32, _I32, _I32, _INT, _INT]
+    lib.estp_attn_importance_ex.restype = _INT
+    lib.estp_attn_importance_ex.argtypes = [_P, _P, _P, _P, _I32, _I32, _I64, _I32, _I32, _I32, _I32, _F, _P, _INT,
+                                            _INT, _P, _P, _SZ, _P]
     lib.estp_combine_pool_workspace_size.restype = _SZ
     lib.estp_combine_pool_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _INT]
     lib.estp_combine_pool.restype = _INT
@@ -236,6 +243,51 @@ def attn_importance_from_lse(Q: torch.Tensor, K: torch.Tensor, lse: torch.Tensor
                                              L, Hq, Hkv, dh, float(scale), dt, _ptr(S), _ptr(workspace), wsb,
                                              _stream(stream)),
            "estp_attn_importance_from_lse")
+    return S
+
+
+def attn_importance_ex(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, max_seqlen: int,
+                       lse: Optional[torch.Tensor] = None, layer_weights=None, exclude_self: bool = False,
+                       scale: Optional[float] = None, S: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Eq. 1 importance with the variants of estp_attn_importance_ex: optional prefill row LSEs
+    ``lse`` [L, Hq, n_tok], per-layer weights (host sequence of L floats), and the diagonal
+    left out of the column sums (``exclude_self``)."""
+    lib = load()
+    if Q.dim() == 3:
+        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
+    _need(Q, "Q", ndim=4)
+    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
+    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
+    L, n_tok, Hq, dh = Q.shape
+    Hkv = K.shape[2]
+    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
+        raise ValueError("Q and K shapes disagree")
+    if lse is not None:
+        if lse.dim() == 2:
+            lse = lse.unsqueeze(0)
+        _need(lse, "lse", device=Q.device, dtype=torch.float32, ndim=3)
+        if tuple(lse.shape) != (L, Hq, n_tok):
+            raise ValueError(f"lse must be [L, Hq, n_tok] = {(L, Hq, n_tok)}")
+    lw = None
+    if layer_weights is not None:
+        if len(layer_weights) != L:
+            raise ValueError(f"layer_weights must hold L = {L} values")
+        lw = (ctypes.c_float * L)(*[float(x) for x in layer_weights])
+    B = cu_seqlens.numel() - 1
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    if S is None:
+        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+    _need(S, "S", device=Q.device, dtype=torch.float32)
+    dt = _dtype_code(Q)
+    ws = lib.estp_attn_importance_ex_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt, int(lse is not None))
+    workspace, wsb = _workspace(ws, Q.device, workspace)
+    flags = ESTP_IMPORTANCE_EXCLUDE_SELF if exclude_self else 0
+    _check(lib.estp_attn_importance_ex(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L,
+                                       Hq, Hkv, dh, float(scale), lw, flags, dt, _ptr(S), _ptr(workspace), wsb,
+                                       _stream(stream)),
+           "estp_attn_importance_ex")
     return S
 
 

@@ -203,7 +203,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
                                                                const int* __restrict__ cu, int B, int n_tok,
                                                                int L, int Hq, int Hkv, float c2,
                                                                const float* __restrict__ lse2, float lse_mul,
-                                                               float* __restrict__ part) {
+                                                               int strict, float* __restrict__ part) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
   constexpr int kTileBytes = kQTile * T::kRowBytes;
@@ -294,7 +294,8 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
       }
       // acc[rb][cb][r]: query i0 + rb*32 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
       const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
-      const bool diag = i0 < k0 + kKPerWave - 1;
+      // tiles holding some query i <= (or, strict, ==) a key of this wave need the mask
+      const bool diag = i0 < k0 + kKPerWave - 1 + strict;
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb) {
         float lr[16];
@@ -315,7 +316,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
             for (int r = 0; r < 16; ++r) {
               const int i = i0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
               const float p = fast_exp2(fmaf(acc[rb][cb][r], c2, -lr[r]));
-              cs += (j <= i) ? p : 0.f;
+              cs += (j < i + 1 - strict) ? p : 0.f;
             }
           } else {
 #pragma unroll
@@ -336,22 +337,33 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   }
 }
 
-// S_j = (sum over layers and KV heads of the column masses) / (N * Hq)
+constexpr int kMaxWeightedLayers = 64;
+struct LayerWeights {
+  float w[kMaxWeightedLayers];
+};
+
+// S_j = (sum over layers l and KV heads of w_l times the column masses) / (N * Hq)
 __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restrict__ part, const int* __restrict__ cu,
-                                                          int n_tok, int LHkv, int Hq, float* __restrict__ S) {
+                                                          int n_tok, int L, int Hkv, int Hq, int weighted,
+                                                          LayerWeights lw, float* __restrict__ S) {
   const int b = blockIdx.y;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= N) return;
   float v = 0.f;
-  for (int k = 0; k < LHkv; ++k) v += part[size_t(k) * n_tok + base + j];
+  for (int l = 0; l < L; ++l) {
+    float vl = 0.f;
+    for (int g = 0; g < Hkv; ++g) vl += part[(size_t(l) * Hkv + g) * n_tok + base + j];
+    v = weighted ? fmaf(lw.w[l], vl, v) : v + vl;
+  }
   S[base + j] = v / (float(N) * float(Hq));
 }
 
 template <int DH>
 void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
-            int Hkv, float scale, const float* lse_in, float* S, float* lse2, float* part, hipStream_t s) {
+            int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S, float* lse2,
+            float* part, hipStream_t s) {
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
   const int nkb = (max_seqlen + kKBlock - 1) / kKBlock;
@@ -364,8 +376,12 @@ void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_
                                                                                    nqb, c2, lse2);
   }
   attn_colsum_kernel<DH><<<dim3(size_t(nkb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
-                                                                                    c2, lse2, lse_mul, part);
-  attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L * Hkv, Hq, S);
+                                                                                    c2, lse2, lse_mul, strict, part);
+  LayerWeights lw{};
+  if (layer_weights)
+    for (int l = 0; l < L; ++l) lw.w[l] = layer_weights[l];
+  attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L, Hkv, Hq,
+                                                                             layer_weights ? 1 : 0, lw, S);
 }
 
 }  // namespace detail
@@ -398,11 +414,12 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
 }
 
 void launch_dh(int dh, const uint16_t* q, const uint16_t* k, const int* cu, int B, int max_seqlen, int n, int L,
-               int Hq, int Hkv, float scale, const float* lse_in, float* S, float* lse2, float* part, hipStream_t s) {
+               int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* lw, float* S, float* lse2,
+               float* part, hipStream_t s) {
   switch (dh) {
-    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
-    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
-    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, S, lse2, part, s); break;
+    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
+    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
+    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
   }
 }
 
@@ -439,7 +456,7 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, nullptr, S, lse2, part, static_cast<hipStream_t>(stream));
+            int(n_tok), L, Hq, Hkv, scale, nullptr, 0, nullptr, S, lse2, part, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance");
   return ESTP_OK;
 }
@@ -476,7 +493,46 @@ extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const
   Carver c(workspace);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, lse, S, nullptr, part, static_cast<hipStream_t>(stream));
+            int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance_from_lse");
+  return ESTP_OK;
+}
+
+extern "C" size_t estp_attn_importance_ex_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L,
+                                                         int32_t Hq, int32_t Hkv, int32_t dh, int dtype,
+                                                         int with_lse) {
+  return with_lse ? estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dtype)
+                  : estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dtype);
+}
+
+extern "C" int estp_attn_importance_ex(const void* Q, const void* K, const float* lse, const int32_t* cu_seqlens,
+                                       int32_t B, int32_t max_seqlen, int64_t n_tok, int32_t L, int32_t Hq,
+                                       int32_t Hkv, int32_t dh, float scale, const float* layer_weights, int flags,
+                                       int dtype, float* S, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  const int st = check_importance_args("estp_attn_importance_ex", Q, K, cu_seqlens, B, max_seqlen, n_tok, L, Hq, Hkv,
+                                       dh, scale, dtype, S);
+  if (st != ESTP_OK) return st;
+  ESTP_REQUIRE((flags & ~ESTP_IMPORTANCE_EXCLUDE_SELF) == 0, ESTP_ERR_INVALID_ARG,
+               "estp_attn_importance_ex: unknown flags 0x%x", flags);
+  ESTP_REQUIRE(!layer_weights || L <= kMaxWeightedLayers, ESTP_ERR_UNSUPPORTED,
+               "estp_attn_importance_ex: at most %d weighted layers, got %d", kMaxWeightedLayers, L);
+  if (layer_weights)
+    for (int l = 0; l < L; ++l)
+      ESTP_REQUIRE(layer_weights[l] == layer_weights[l] && fabsf(layer_weights[l]) < INFINITY, ESTP_ERR_INVALID_ARG,
+                   "estp_attn_importance_ex: layer weight %d is not finite", l);
+  const size_t need =
+      estp_attn_importance_ex_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dtype, lse != nullptr);
+  ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
+               "estp_attn_importance_ex: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
+               "estp_attn_importance_ex: workspace must be non-null and 256-byte aligned");
+  Carver c(workspace);
+  float* lse2 = lse ? nullptr : c.take<float>(size_t(L) * Hq * n_tok);
+  float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+            int(n_tok), L, Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S,
+            lse2, part, static_cast<hipStream_t>(stream));
+  ESTP_CHECK_LAUNCH("estp_attn_importance_ex");
   return ESTP_OK;
 }

@@ -210,3 +210,30 @@ def test_head_train_step_validation():
     assert call(eps=0.0) == 1
     assert call(theta=UNALIGNED) == 1
     assert call(wsb=ws - 1) == 3
+
+
+@needs_no_gpu
+def test_importance_ex_validation():
+    lib = estp.load()
+    ws2 = lib.estp_attn_importance_ex_workspace_size(100, 2, 60, 2, 4, 2, 64, 0, 0)
+    ws1 = lib.estp_attn_importance_ex_workspace_size(100, 2, 60, 2, 4, 2, 64, 0, 1)
+    assert ws2 == lib.estp_attn_importance_workspace_size(100, 2, 60, 2, 4, 2, 64, 0)
+    assert ws1 == lib.estp_attn_importance_from_lse_workspace_size(100, 2, 60, 2, 4, 2, 64, 0)
+    w2 = (ctypes.c_float * 2)(1.0, 0.5)
+    base = [FAKE, FAKE, None, FAKE, 2, 60, 100, 2, 4, 2, 64, 0.125, w2, 1, 0, FAKE, WS, ws2, None]
+
+    def call(**kw):
+        a = list(base)
+        idx = {"Q": 0, "lse": 2, "B": 4, "L": 7, "dh": 10, "lw": 12, "flags": 13, "wsb": 17}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.estp_attn_importance_ex(*a)
+
+    assert call(Q=None) == 1
+    assert call(B=0) == 1
+    assert call(flags=4) == 1
+    assert call(lw=(ctypes.c_float * 2)(1.0, float("nan"))) == 1
+    assert call(dh=96) == 2
+    assert call(L=65, lw=(ctypes.c_float * 65)(*([1.0] * 65))) == 2  # more weighted layers than supported
+    assert call(wsb=ws2 - 1) == 3
+    assert call(lse=FAKE, wsb=ws1 - 1) == 3

@@ -143,6 +143,30 @@ def test_importance_from_lse_uses_the_given_normalisers():
     assert not np.allclose(ref, oracle.attn_importance(Q, K, cu), rtol=1e-2)
 
 
+@pytest.mark.parametrize("lengths,L,Hq,Hkv,dh,qs,tag", IMPORTANCE_CASES, ids=[c[-1] for c in IMPORTANCE_CASES])
+def test_importance_ex_variants_parity(lengths, L, Hq, Hkv, dh, qs, tag):
+    # diagonal left out of the column sums, per-layer weights, with and without given row LSEs
+    Q, K, cu = _qk(lengths, L, Hq, Hkv, dh, qs, 5)
+    Qd, Kd, cud = dev(Q), dev(K), dev(cu)
+    w = [1.5 - 0.75 * l for l in range(L)]
+    ref_ex = oracle.attn_importance(Q, K, cu, exclude_self=True)
+    ref_w = oracle.attn_importance(Q, K, cu, layer_weights=w)
+    ref_both = oracle.attn_importance(Q, K, cu, exclude_self=True, layer_weights=w)
+    lse = dev(oracle.attn_row_lse(Q, K, cu).astype(np.float32))
+    tol = lambda ref: S_RTOL * np.abs(ref) + 1e-6 * np.abs(ref).max()
+    for with_lse in (False, True):
+        kw = {"lse": lse} if with_lse else {}
+        got = host(estp.attn_importance_ex(Qd, Kd, cud, max(lengths), exclude_self=True, **kw))
+        assert np.all(np.abs(got - ref_ex) <= tol(ref_ex))
+        got = host(estp.attn_importance_ex(Qd, Kd, cud, max(lengths), layer_weights=w, **kw))
+        assert np.all(np.abs(got - ref_w) <= tol(ref_w))
+        got = host(estp.attn_importance_ex(Qd, Kd, cud, max(lengths), layer_weights=w, exclude_self=True, **kw))
+        assert np.all(np.abs(got - ref_both) <= tol(ref_both))
+    # with no variant the extended call is the plain one
+    plain = host(estp.attn_importance(Qd, Kd, cud, max(lengths)))
+    assert np.array_equal(host(estp.attn_importance_ex(Qd, Kd, cud, max(lengths))), plain)
+
+
 def test_importance_repeatable_bitwise():
     Q, K, cu = _qk([300, 45, 600], 2, 8, 2, 128, 1.0, 6)
     Qd, Kd, cud = dev(Q), dev(K), dev(cu)
