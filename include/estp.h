@@ -66,8 +66,9 @@ typedef enum estp_dtype { ESTP_BF16 = 0, ESTP_F32 = 1 } estp_dtype;
 
 /* How S and H are scaled before Eq. 3.  NONE is Eq. 3 as printed; ZSCORE
  * replaces S and H by their per-prompt z-scores (population standard
- * deviation, (v - mean) / (std + 1e-6)) so that both terms are commensurate. */
-typedef enum estp_norm { ESTP_NORM_NONE = 0, ESTP_NORM_ZSCORE = 1 } estp_norm;
+ * deviation, (v - mean) / (std + 1e-6)) so that both terms are commensurate;
+ * MINMAX by (v - min) / (max - min + 1e-6) per prompt. */
+typedef enum estp_norm { ESTP_NORM_NONE = 0, ESTP_NORM_ZSCORE = 1, ESTP_NORM_MINMAX = 2 } estp_norm;
 
 /* Hidden activation of the length head (the paper names an MLP predictor
  * without fixing its activation). */

@@ -21,7 +21,8 @@ reason in the design notes of the repository):
   queries and keys; query head h reads key head ``h // (Hq // Hkv)``.
 * Eq. 4 is read with the temperature the text names: e = softmax(T / alpha).
 * ``norm="zscore"`` replaces S and H by their per-prompt z-scores before
-  Eq. 3 (population std, epsilon 1e-6); ``norm="none"`` is Eq. 3 literally.
+  Eq. 3 (population std, epsilon 1e-6); ``norm="minmax"`` by
+  (v - min) / (max - min + 1e-6) per prompt; ``norm="none"`` is Eq. 3 literally.
 * ties (top token, bin argmax) go to the lowest index; the shortest-job-first
   order is a stable ascending sort of y-hat.
 """
@@ -241,6 +242,10 @@ def _zscore(v: np.ndarray, eps: float = 1e-6) -> np.ndarray:
     return (v - v.mean()) / (v.std() + eps)
 
 
+def _minmax(v: np.ndarray, eps: float = 1e-6) -> np.ndarray:
+    return (v - v.min()) / (v.max() - v.min() + eps)
+
+
 def combine_weights(S, H, cu_seqlens, lambda1: float, lambda2: float, alpha: float = 1.0,
                     norm: str = "none"):
     """T_i = lambda1 S_i + lambda2 H_i (Eq. 3); e = softmax over the prompt of T / alpha (Eq. 4).
@@ -260,6 +265,8 @@ def combine_weights(S, H, cu_seqlens, lambda1: float, lambda2: float, alpha: flo
         s, h = S[lo:hi], H[lo:hi]
         if norm == "zscore":
             s, h = _zscore(s), _zscore(h)
+        elif norm == "minmax":
+            s, h = _minmax(s), _minmax(h)
         elif norm != "none":
             raise ValueError(norm)
         T = lambda1 * s + lambda2 * h

@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("ESTP_LIBRARY") or os.path.join(_HERE, "libestp.so")
 ESTP_OK, ESTP_ERR_INVALID_ARG, ESTP_ERR_UNSUPPORTED, ESTP_ERR_WORKSPACE, ESTP_ERR_HIP = range(5)
 ESTP_BF16, ESTP_F32 = 0, 1
 ESTP_IMPORTANCE_EXCLUDE_SELF = 1
-NORMS = {"none": 0, "zscore": 1}
+NORMS = {"none": 0, "zscore": 1, "minmax": 2}
 ACTS = {"relu": 0, "gelu_tanh": 1}
 
 EXPORTS = (

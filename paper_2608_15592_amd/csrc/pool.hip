@@ -6,12 +6,14 @@
 // u_i = T_i / alpha for its rows, the chunk's own max m_c (and first arg-max),
 // p_i = exp(u_i - m_c) and exp-sum s_c with wave reductions only, and streams
 // X once: each thread owns 8 consecutive hidden features (one 16-byte bf16
-// load per row, 8 rows in flight) and accumulates sum_i p_i x_i in fp32.  pool_finish_kernel combines the chunks of each
-// prompt in a fixed order, weighting chunk c by exp(m_c - M) / Z (M the prompt
-// max, Z its exp-sum), which is exactly sum_i e_i x_i; it also writes the
-// arg-max token and, when asked, the normalised weights e.  With z-scored
-// inputs a per-prompt statistics pass (zscore_stats_kernel) runs first.  No
-// atomics: results are bitwise reproducible.
+// load per row, 8 rows in flight) and accumulates sum_i p_i x_i in fp32.
+// pool_finish_kernel combines the chunks of each prompt in a fixed order,
+// weighting chunk c by exp(m_c - M) / Z (M the prompt max, Z its exp-sum),
+// which is exactly sum_i e_i x_i; it also writes the arg-max token and, when
+// asked, the normalised weights e.  With z-scored or min-max scaled inputs a
+// per-prompt statistics pass (zscore_stats_kernel, minmax_stats_kernel) runs
+// first and folds the scaling into u = a1 S + a2 H + c0.  No atomics: results
+// are bitwise reproducible.
 #include "estp_common.h"
 
 namespace estp {
@@ -96,6 +98,45 @@ __global__ __launch_bounds__(1024) void zscore_stats_kernel(const float* __restr
   if (threadIdx.x == 0) {
     const float c1 = a1 / (sds + kZEps), c2 = a2 / (sdh + kZEps);
     coef[b] = make_float4(c1, c2, -(c1 * ms + c2 * mh), 0.f);
+  }
+}
+
+__device__ float block_reduce_max(float v, float* sh) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float r = -INFINITY;
+  const int nw = blockDim.x >> 6;
+  for (int i = 0; i < nw; ++i) r = fmaxf(r, sh[i]);
+  return r;
+}
+
+// Per-prompt coefficients of u = a1 S + a2 H + c0 for min-max scaled inputs:
+// (lambda1 (S - min_S) / (max_S - min_S + eps) + lambda2 (H - min_H) / (max_H - min_H + eps)) / alpha.
+__global__ __launch_bounds__(1024) void minmax_stats_kernel(const float* __restrict__ S, const float* __restrict__ H,
+                                                            const int* __restrict__ cu, float a1, float a2,
+                                                            float4* __restrict__ coef) {
+  __shared__ float sh[16];
+  const int b = blockIdx.x;
+  const int base = cu[b];
+  const int N = cu[b + 1] - base;
+  float xs = -INFINITY, ns = -INFINITY, xh = -INFINITY, nh = -INFINITY;  // max and -min
+  for (int i = threadIdx.x; i < N; i += blockDim.x) {
+    const float sv = S[base + i], hv = H[base + i];
+    xs = fmaxf(xs, sv);
+    ns = fmaxf(ns, -sv);
+    xh = fmaxf(xh, hv);
+    nh = fmaxf(nh, -hv);
+  }
+  xs = block_reduce_max(xs, sh);
+  ns = block_reduce_max(ns, sh);
+  xh = block_reduce_max(xh, sh);
+  nh = block_reduce_max(nh, sh);
+  if (threadIdx.x == 0) {
+    const float c1 = a1 / ((xs + ns) + kZEps), c2 = a2 / ((xh + nh) + kZEps);
+    coef[b] = make_float4(c1, c2, c1 * ns + c2 * nh, 0.f);
   }
 }
 
@@ -323,7 +364,7 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
                "estp_combine_pool: alpha must be finite and > 0");
   ESTP_REQUIRE(lambda1 == lambda1 && lambda2 == lambda2 && fabsf(lambda1) < INFINITY && fabsf(lambda2) < INFINITY,
                ESTP_ERR_INVALID_ARG, "estp_combine_pool: lambda1 and lambda2 must be finite");
-  ESTP_REQUIRE(norm == ESTP_NORM_NONE || norm == ESTP_NORM_ZSCORE, ESTP_ERR_INVALID_ARG,
+  ESTP_REQUIRE(norm == ESTP_NORM_NONE || norm == ESTP_NORM_ZSCORE || norm == ESTP_NORM_MINMAX, ESTP_ERR_INVALID_ARG,
                "estp_combine_pool: unknown norm %d", norm);
   ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG, "estp_combine_pool: unknown dtype %d",
                dtype);
@@ -349,6 +390,10 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
   if (norm == ESTP_NORM_ZSCORE) {
     zscore_stats_kernel<<<dim3(B), dim3(1024), 0, s>>>(S, H, cu_seqlens, a1, a2, coef);
     ESTP_CHECK_LAUNCH("zscore_stats_kernel");
+    cf = coef;
+  } else if (norm == ESTP_NORM_MINMAX) {
+    minmax_stats_kernel<<<dim3(B), dim3(1024), 0, s>>>(S, H, cu_seqlens, a1, a2, coef);
+    ESTP_CHECK_LAUNCH("minmax_stats_kernel");
     cf = coef;
   }
   const dim3 grid(nch, B, nslices);

@@ -182,7 +182,7 @@ COMBINE_GRID = [(0.1, 0.9, 1.0), (0.5, 0.5, 0.5), (0.9, 0.1, 2.0), (0.0, 0.0, 1.
 
 
 @pytest.mark.parametrize("xdtype", ["bf16", "f32"])
-@pytest.mark.parametrize("norm", ["none", "zscore"])
+@pytest.mark.parametrize("norm", ["none", "zscore", "minmax"])
 def test_combine_pool_parity(xdtype, norm):
     lengths = [1, 7, 256, 257, 600, 33]
     n = sum(lengths)

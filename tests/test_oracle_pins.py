@@ -629,3 +629,18 @@ def test_importance_layer_weights_linear():
     per_layer = [oracle.attn_importance(Q[l:l + 1], K[l:l + 1], cu) for l in range(3)]
     np.testing.assert_allclose(oracle.attn_importance(Q, K, cu, layer_weights=w),
                                sum(wl * s for wl, s in zip(w, per_layer)), rtol=1e-13)
+
+
+def test_combine_minmax_closed_forms():
+    # min-max scaling maps each prompt's S and H onto [0, 1) affinely: weights follow by hand
+    S = np.array([2.0, 4.0, 3.0, 7.0, 7.0])
+    H = np.array([1.0, 0.0, 5.0, 2.0, 2.0])
+    cu = [0, 3, 5]
+    e, top = oracle.combine_weights(S, H, cu, 0.6, 0.4, 0.5, "minmax")
+    s0 = (S[:3] - 2.0) / (2.0 + 1e-6)
+    h0 = (H[:3] - 0.0) / (5.0 + 1e-6)
+    u = (0.6 * s0 + 0.4 * h0) / 0.5
+    np.testing.assert_allclose(e[:3], np.exp(u) / np.exp(u).sum(), rtol=1e-13)
+    # a constant prompt (zero range) scales to zeros: uniform weights, first index on top
+    np.testing.assert_allclose(e[3:], [0.5, 0.5], rtol=1e-15)
+    assert top[1] == 3
