@@ -161,8 +161,9 @@ def main() -> int:
     t0 = time.time()
     X, W, Q, K = (to_dev(inp[k], torch) for k in ("X", "W", "Q", "K"))
     cu = to_dev(inp["cu_seqlens"], torch)
-    head = tuple(to_dev(inp[k], torch) for k in ("W1", "b1", "W2", "b2"))
     Hdn, n_bins = w.head
+    head = tuple(to_dev(inp[k], torch) for k in ("W1", "b1", "W2", "b2")) + (
+        to_dev(inp["centres"], torch) if n_bins > 1 else None,)
     torch.cuda.synchronize()
     log(f"uploaded in {time.time() - t0:.1f} s")
     bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, n_bins, X.device)
@@ -182,7 +183,7 @@ def main() -> int:
                                          workspace=bufs["ws_pool"], stream=stream)
         if evs:
             evs[3].record(stream)
-        estp.predict(pooled, *head, None, workspace=bufs["ws_predict"], stream=stream)
+        estp.predict(pooled, *head, workspace=bufs["ws_predict"], stream=stream)
         if evs:
             evs[4].record(stream)
 

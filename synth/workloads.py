@@ -55,6 +55,12 @@ WORKLOADS = {
         description=("ragged RL batch: 256 prompts, lengths log-uniform in [32, 4096], Llama-3-8B shapes, "
                      "packed varlen, 4096->1024->1 length head, bf16"),
     ),
+    "llama1b": Workload(
+        name="llama1b", n_prompts=32, seq_len=2048, d=2048, V=128256, Hq=32, Hkv=8, dh=64, L=4,
+        outlier_frac=0.05, head=(1024, 16),
+        description=("Llama-3.2-1B-shaped: 32 x 2048 tokens, d=2048, V=128256, 32/8 heads of 64, "
+                     "importance summed over 4 layers, 5% x4-norm outlier tokens, 16-bin head, bf16"),
+    ),
     "long": Workload(
         name="long", n_prompts=2, seq_len=32768, d=4096, V=128256, Hq=32, Hkv=8, dh=128, L=1,
         outlier_frac=0.05,

@@ -34,7 +34,7 @@ def _run(w, seed=42):
     Hdn, K = w.head
     X, W, Q, Kk = (dev(inp[k]) for k in ("X", "W", "Q", "K"))
     cu = dev(inp["cu_seqlens"])
-    head = tuple(dev(inp[k]) for k in ("W1", "b1", "W2", "b2")) + (None,)
+    head = tuple(dev(inp[k]) for k in ("W1", "b1", "W2", "b2")) + (dev(inp["centres"]) if K > 1 else None,)
     bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, K, X.device)
     out = estp.run_path(X, W, Q, Kk, cu, max_len, LAM1, LAM2, ALPHA, "none", head=head, bufs=bufs)
     torch.cuda.synchronize()
@@ -121,6 +121,15 @@ def test_fullsize_llama_shaped():
     _entropy_rows(inp, got)
     _properties(inp, got, w)
     _exact_prompt(inp, got, w, 0)
+
+
+def test_fullsize_llama1b_shaped():
+    # head_dim 64 attention, d = 2048, 16-bin head
+    w = synth.get_workload("llama1b")
+    inp, got = _run(w)
+    _entropy_rows(inp, got)
+    _properties(inp, got, w)
+    _exact_prompt(inp, got, w, 3)
 
 
 def test_fullsize_ragged_rl_batch():
