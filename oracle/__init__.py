@@ -19,6 +19,8 @@ exactly to float64 and evaluates the paper's definitions:
 * ``soft_labels``, ``length_loss`` - Eq. 6 and Eq. 8 (Section 4.3)
 * ``length_bin``, ``head_loss_and_grads``, ``adamw_step``, ``head_train_step`` - one
   training step of the K-bin head: Eq. 8 loss, its gradients, AdamW (Section 5.1)
+* ``misalignment_counts`` - the entropy / semantics percentile split (Fig. 1b, Section 1)
+* ``sjf_padding``        - padding and completion time of static SJF batches (Section 5.4)
 
 ``oracle.bruteforce`` re-derives the same quantities with pure-Python loops
 for tiny shapes; the tests pin this module against it, against closed forms
@@ -40,5 +42,7 @@ from .estp_oracle import (  # noqa: F401
     head_loss_and_grads,
     adamw_step,
     head_train_step,
+    misalignment_counts,
+    sjf_padding,
     run_path,
 )

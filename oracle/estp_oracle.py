@@ -434,6 +434,59 @@ def head_train_step(pooled, y, edges, centres, params, m, v, t: int, lambda3: fl
     return loss, g, P, M, Vv
 
 
+# ----------------------------------------------------------------------------- analyses on the outputs
+
+def _rank_sets(v: np.ndarray, frac_low: float, frac_high: float):
+    """Token sets of one prompt by rank of v (ascending, ties by lower index first): the
+    floor(frac_low N) lowest and the floor(frac_high N) highest."""
+    N = len(v)
+    order = np.argsort(np.asarray(v, dtype=np.float64), kind="stable")
+    nl, nh = int(math.floor(frac_low * N)), int(math.floor(frac_high * N))
+    low = np.zeros(N, dtype=bool)
+    high = np.zeros(N, dtype=bool)
+    low[order[:nl]] = True
+    high[order[N - nh:]] = True
+    return low, high
+
+
+def misalignment_counts(H, S, cu_seqlens, frac_low: float = 0.4, frac_high: float = 0.4) -> np.ndarray:
+    """Entropy-semantics misalignment of each prompt (the diagnostic behind Fig. 1b, Section 1):
+    tokens are split by rank within the prompt into the top ``frac_high`` and the bottom
+    ``frac_low`` of H and of S.  Returns int64 [B, 4]: (#high-H, #high-H that are low-S,
+    #low-H, #low-H that are high-S); the two misalignment ratios are columns 1/0 and 3/2."""
+    H = np.asarray(H, dtype=np.float64)
+    S = np.asarray(S, dtype=np.float64)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    out = np.zeros((len(cu) - 1, 4), dtype=np.int64)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        lowH, highH = _rank_sets(H[lo:hi], frac_low, frac_high)
+        lowS, highS = _rank_sets(S[lo:hi], frac_low, frac_high)
+        out[b] = [highH.sum(), (highH & lowS).sum(), lowH.sum(), (lowH & highS).sum()]
+    return out
+
+
+def sjf_padding(lengths, order, batch: int):
+    """Static batches of ``batch`` requests taken in ``order`` (e.g. the shortest-job-first order
+    of the predicted lengths, Section 5.4); each batch runs for its longest true length.
+    Returns ``(padded, useful, jct_sum)`` as integers: padded tokens sum_batches
+    (size * max - sum), useful tokens sum y, and the sum over requests of the completion time
+    start(batch) + y_i with batches run back to back.  Padding ratio = padded / useful;
+    mean JCT = jct_sum / B."""
+    y = np.asarray(lengths, dtype=np.int64)
+    order = np.arange(len(y)) if order is None else np.asarray(order, dtype=np.int64)
+    padded = useful = jct = 0
+    start = 0
+    for k0 in range(0, len(order), batch):
+        members = y[order[k0:k0 + batch]]
+        mx = int(members.max())
+        padded += len(members) * mx - int(members.sum())
+        useful += int(members.sum())
+        jct += len(members) * start + int(members.sum())
+        start += mx
+    return padded, useful, jct
+
+
 # ----------------------------------------------------------------------------- whole path
 
 def run_path(X, W, Q, K, cu_seqlens, lambda1: float, lambda2: float, alpha: float = 1.0,

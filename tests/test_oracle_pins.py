@@ -644,3 +644,46 @@ def test_combine_minmax_closed_forms():
     # a constant prompt (zero range) scales to zeros: uniform weights, first index on top
     np.testing.assert_allclose(e[3:], [0.5, 0.5], rtol=1e-15)
     assert top[1] == 3
+
+
+# ============================================================================ analyses
+
+def test_misalignment_by_hand():
+    # N = 10, 40% -> 4 tokens in each of the high and low sets; ranks read off directly
+    H = np.array([9, 8, 7, 6, 5, 4, 3, 2, 1, 0], dtype=float)      # high H: tokens 0-3, low H: 6-9
+    S = np.array([0, 1, 9, 8, 5, 5, 7, 2, 3, 4], dtype=float)      # low S: 0, 1, 7, 8; high S: 2, 3, 6, 5
+    c = oracle.misalignment_counts(H, S, [0, 10])
+    # the tied 5s rank 4 before 5, so token 5 is in the top four of S and token 4 is not
+    # high-H {0,1,2,3} & low-S {0,1,7,8} = {0,1}; low-H {6,7,8,9} & high-S {2,3,5,6} = {6}
+    assert c.tolist() == [[4, 2, 4, 1]]
+    # ties go by index: equal values, the lower index ranks lower
+    c = oracle.misalignment_counts(np.zeros(5), np.arange(5.0), [0, 5], 0.4, 0.4)
+    # H all equal: low-H = tokens 0,1 (lowest indices), high-H = tokens 3,4; S low = 0,1, high = 3,4
+    assert c.tolist() == [[2, 0, 2, 0]]
+
+
+def test_misalignment_bruteforce_ranks():
+    g = _rng(80)
+    H = g.integers(0, 5, size=23).astype(float)   # many ties
+    S = g.standard_normal(23)
+    cu = [0, 9, 23]
+    got = oracle.misalignment_counts(H, S, cu, 0.3, 0.5)
+    for b, (lo, hi) in enumerate(((0, 9), (9, 23))):
+        N = hi - lo
+        rank = lambda v, i: sum(1 for j in range(lo, hi) if (v[j], j) < (v[i], i))   # lexicographic
+        nl, nh = int(0.3 * N), int(0.5 * N)
+        lowH = {i for i in range(lo, hi) if rank(H, i) < nl}
+        highH = {i for i in range(lo, hi) if rank(H, i) >= N - nh}
+        lowS = {i for i in range(lo, hi) if rank(S, i) < nl}
+        highS = {i for i in range(lo, hi) if rank(S, i) >= N - nh}
+        assert got[b].tolist() == [len(highH), len(highH & lowS), len(lowH), len(lowH & highS)]
+
+
+def test_sjf_padding_by_hand():
+    y = [5, 1, 9, 2]
+    # arrival order, batches of 2: (5,1) max 5, (9,2) max 9
+    assert oracle.sjf_padding(y, None, 2) == (4 + 7, 17, (5 + 1) + (2 * 5 + 11))
+    # shortest first: (1,2) max 2, (5,9) max 9
+    assert oracle.sjf_padding(y, [1, 3, 0, 2], 2) == (1 + 4, 17, (1 + 2) + (2 * 2 + 14))
+    # a ragged last batch
+    assert oracle.sjf_padding([3, 3, 3], None, 2) == (0, 9, (3 + 3) + (3 + 3))
