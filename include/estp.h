@@ -260,6 +260,35 @@ ESTP_API int estp_head_train_step(const float* pooled, const float* y, int32_t B
                          int32_t step, float lambda3, float lr, float beta1, float beta2, float eps,
                          float weight_decay, float* loss, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Analyses on the path's outputs.
+ *
+ * estp_misalignment: the entropy / semantics split behind Fig. 1b
+ * (Section 1).  Within each prompt (N tokens) the tokens are ranked by H and
+ * by S (ascending; equal values by token index) and split into the lowest
+ * floor(frac_low N) and the highest floor(frac_high N) (the paper's 60th
+ * percentile split is frac_low = frac_high = 0.4).
+ *   H, S [n_tok]    float32, device;  cu_seqlens [B+1] int32, device
+ *   counts [B, 4]   int32 output: #high-H, #high-H that are low-S,
+ *                   #low-H, #low-H that are high-S
+ * The two misalignment ratios are counts[.,1] / counts[.,0] and
+ * counts[.,3] / counts[.,2].  Exact integer counts.
+ *
+ * estp_sjf_padding: static batches of `batch` requests taken in `order`
+ * (e.g. the shortest-job-first order from estp_predict, Section 5.4; NULL =
+ * as given); each batch runs for its longest true length, back to back.
+ *   lengths [B]     int32 true output lengths, device
+ *   order [B]       int32 permutation of 0..B-1, device, or NULL
+ *   out [3]         int64 output, device: padded tokens
+ *                   sum_batches (size * max - sum), useful tokens sum y,
+ *                   sum over requests of start(batch) + y_i
+ * Padding ratio = out[0] / out[1]; mean completion time = out[2] / B.
+ * ------------------------------------------------------------------------ */
+ESTP_API int estp_misalignment(const float* H, const float* S, const int32_t* cu_seqlens, int32_t B, float frac_low,
+                      float frac_high, int32_t* counts, void* stream);
+ESTP_API int estp_sjf_padding(const int32_t* lengths, const int32_t* order, int32_t B, int32_t batch, int64_t* out,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

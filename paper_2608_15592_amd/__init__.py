@@ -9,6 +9,7 @@ Python face of libestp.so: the four calls of the ESTP path (arXiv 2608.15592)
 * ``combine_pool``    - Eq. 3-5, temperature softmax of the fused score and weighted pooling
 * ``predict``         - length head (Section 4.3, Eq. 7) and shortest-job-first order
 * ``head_train_step`` - one Eq. 6-8 / AdamW training step of the K-bin head
+* ``misalignment``, ``sjf_padding`` - the Fig. 1b rank split and static SJF batch padding / JCT
 
 plus ``run_path`` chaining them.  All computation runs in the library's HIP
 kernels; torch only supplies device memory and the stream.
@@ -25,6 +26,8 @@ from ._lib import (  # noqa: F401
     predict,
     head_param_views,
     head_train_step,
+    misalignment,
+    sjf_padding,
     token_entropy,
     token_entropy_workspace_size,
 )

@@ -33,6 +33,7 @@ EXPORTS = (
     "estp_combine_pool_workspace_size", "estp_combine_pool",
     "estp_predict_workspace_size", "estp_predict",
     "estp_head_train_step_workspace_size", "estp_head_train_step",
+    "estp_misalignment", "estp_sjf_padding",
 )
 
 
@@ -99,6 +100,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_head_train_step.restype = _INT
     lib.estp_head_train_step.argtypes = [_P, _P, _I32, _I32, _I32, _I32, _INT, _P, _P, _P, _P, _P, _I32, _F, _F, _F,
                                          _F, _F, _F, _P, _P, _SZ, _P]
+    lib.estp_misalignment.restype = _INT
+    lib.estp_misalignment.argtypes = [_P, _P, _P, _I32, _F, _F, _P, _P]
+    lib.estp_sjf_padding.restype = _INT
+    lib.estp_sjf_padding.argtypes = [_P, _P, _I32, _I32, _P, _P]
     _lib = lib
     return lib
 
@@ -382,3 +387,30 @@ def head_train_step(pooled: torch.Tensor, y: torch.Tensor, edges: torch.Tensor, 
                                     _ptr(workspace), wsb, _stream(stream)),
            "estp_head_train_step")
     return loss
+
+
+def misalignment(H: torch.Tensor, S: torch.Tensor, cu_seqlens: torch.Tensor, frac_low: float = 0.4,
+                 frac_high: float = 0.4, stream=None) -> torch.Tensor:
+    """Per-prompt counts [B, 4] of the entropy / semantics rank split (Fig. 1b): #high-H,
+    #high-H that are low-S, #low-H, #low-H that are high-S."""
+    lib = load()
+    _need(H, "H", dtype=torch.float32, ndim=1)
+    _need(S, "S", device=H.device, dtype=torch.float32, ndim=1)
+    _need(cu_seqlens, "cu_seqlens", device=H.device, dtype=torch.int32, ndim=1)
+    B = cu_seqlens.numel() - 1
+    counts = torch.empty(B, 4, dtype=torch.int32, device=H.device)
+    _check(lib.estp_misalignment(_ptr(H), _ptr(S), _ptr(cu_seqlens), B, float(frac_low), float(frac_high),
+                                 _ptr(counts), _stream(stream)), "estp_misalignment")
+    return counts
+
+
+def sjf_padding(lengths: torch.Tensor, order: Optional[torch.Tensor], batch: int, stream=None) -> torch.Tensor:
+    """(padded tokens, useful tokens, sum of completion times) of static batches taken in ``order``."""
+    lib = load()
+    _need(lengths, "lengths", dtype=torch.int32, ndim=1)
+    if order is not None:
+        _need(order, "order", device=lengths.device, dtype=torch.int32, ndim=1)
+    out = torch.empty(3, dtype=torch.int64, device=lengths.device)
+    _check(lib.estp_sjf_padding(_ptr(lengths), _ptr(order), lengths.numel(), int(batch), _ptr(out), _stream(stream)),
+           "estp_sjf_padding")
+    return out

@@ -237,3 +237,13 @@ def test_importance_ex_validation():
     assert call(L=65, lw=(ctypes.c_float * 65)(*([1.0] * 65))) == 2  # more weighted layers than supported
     assert call(wsb=ws2 - 1) == 3
     assert call(lse=FAKE, wsb=ws1 - 1) == 3
+
+
+@needs_no_gpu
+def test_analysis_validation():
+    lib = estp.load()
+    assert lib.estp_misalignment(None, FAKE, FAKE, 2, 0.4, 0.4, FAKE, None) == 1
+    assert lib.estp_misalignment(FAKE, FAKE, FAKE, 0, 0.4, 0.4, FAKE, None) == 1
+    assert lib.estp_misalignment(FAKE, FAKE, FAKE, 2, 1.5, 0.4, FAKE, None) == 1
+    assert lib.estp_sjf_padding(None, None, 4, 2, FAKE, None) == 1
+    assert lib.estp_sjf_padding(FAKE, None, 4, 0, FAKE, None) == 1

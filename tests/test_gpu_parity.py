@@ -400,3 +400,32 @@ def test_head_train_step_matches_predict_and_learns():
     yhat, _, _ = estp.predict(hd, W1, b1, W2, b2, cd)
     ref, _, _ = oracle.predict(h, host(W1), host(b1), host(W2), host(b2), centres)
     np.testing.assert_allclose(host(yhat), ref, rtol=1e-4)
+
+
+# ------------------------------------------------------------------------------------------ analyses
+
+@pytest.mark.parametrize("frac", [(0.4, 0.4), (0.3, 0.5), (0.0, 1.0), (1.0, 0.0)])
+def test_misalignment_parity(frac):
+    # integer counts: bit-exact against the oracle on the same float32 scores (ties included)
+    g = np.random.default_rng(30)
+    lengths = [1, 2, 5, 64, 257, 1000, 4096, 33]
+    n = sum(lengths)
+    H = g.standard_normal(n).astype(np.float32)
+    S = (g.integers(0, 40, size=n) / 7.0).astype(np.float32)   # many equal values
+    H[100:150] = 0.0
+    cu = I.cu_seqlens_from_lengths(lengths)
+    got = host(estp.misalignment(dev(H), dev(S), dev(cu), *frac))
+    ref = oracle.misalignment_counts(H, S, cu, *frac)
+    assert np.array_equal(got, ref)
+
+
+def test_sjf_padding_parity():
+    g = np.random.default_rng(31)
+    for B, batch in ((1, 1), (7, 3), (1000, 16), (65536, 32)):
+        y = g.integers(1, 20000, size=B).astype(np.int32)
+        yhat = y * np.exp(g.normal(0.0, 0.5, size=B))
+        order = np.argsort(yhat, kind="stable").astype(np.int32)
+        for o in (None, order):
+            got = host(estp.sjf_padding(dev(y), None if o is None else dev(o), batch))
+            ref = oracle.sjf_padding(y, o, batch)
+            assert tuple(int(x) for x in got) == ref
