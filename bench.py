@@ -249,6 +249,28 @@ def main() -> int:
     del theta, m_tr, v_tr
     log(f"head training step (B={B}, {w.d}->{Hd_tr}->{K_tr}): {tr_ms:.3f} ms")
 
+    # The Fig. 1b split on this step's H and S, and the padding of SJF batches of 16 built from
+    # the step's predicted lengths against synthetic true lengths; timed on their own.
+    H_s, S_s = bufs["H"], bufs["S"]
+    yhat_s = estp.predict(bufs["pooled"], *head, workspace=bufs["ws_predict"], stream=stream)
+    y_true = torch.exp(torch.empty(B).uniform_(math.log(16.0), math.log(16384.0), generator=g_tr)).to(
+        torch.int32).to(X.device)
+    an_evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    an_evs[0].record(stream)
+    counts = estp.misalignment(H_s, S_s, cu, stream=stream)
+    an_evs[1].record(stream)
+    pad = estp.sjf_padding(y_true, yhat_s[2], 16, stream=stream)
+    an_evs[2].record(stream)
+    torch.cuda.synchronize()
+    c = counts.sum(dim=0).tolist()
+    pad = pad.tolist()
+    analyses = {"misalignment_ms": an_evs[0].elapsed_time(an_evs[1]),
+                "high_H_low_S_ratio": c[1] / max(1, c[0]), "low_H_high_S_ratio": c[3] / max(1, c[2]),
+                "sjf_padding_ms": an_evs[1].elapsed_time(an_evs[2]), "sjf_padding_ratio": pad[0] / max(1, pad[1]),
+                "note": "40% rank split per prompt on this step's H and S (synthetic inputs); SJF batches of 16 "
+                        "ordered by the predicted lengths, synthetic true lengths"}
+    log(f"analyses: misalignment {analyses['misalignment_ms']:.3f} ms, sjf padding {analyses['sjf_padding_ms']:.3f} ms")
+
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
     pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
@@ -293,6 +315,7 @@ def main() -> int:
         "head_train_step": {"ms": tr_ms, "head": f"{w.d}->{Hd_tr}->{K_tr}", "batch": B, "param_bytes_rw": tr_bytes,
                             "achieved_GBps": tr_bytes / (tr_ms * 1e-3) / 1e9,
                             "note": "estp_head_train_step (Eq. 8 loss, backward, AdamW); not part of the timed step"},
+        "analyses": analyses,
         "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
                     "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
                     "note": "whole combine_pool call (weights + pooling + chunk reduction), warm after importance"},
