@@ -195,3 +195,161 @@ def _predict_mutant(kind):
 @pytest.mark.parametrize("kind", ["descending", "ties_reversed", "argmin_bin", "no_softmax", "no_activation"])
 def test_predict_mutant_caught(kind):
     assert _fails_some(P.PREDICT_PINS, _predict_mutant(kind)), kind
+
+
+# ---------------------------------------------------------------------------- mutants of the later rows
+# Each mutant replaces one oracle function (as the pins reach it, through the package) with a
+# plausible slip; at least one of the listed pins must then fail.
+
+import oracle  # noqa: E402
+
+
+def _row_lse_excl_diag(Q, K, cu, scale=None, row_chunk=2048):
+    Qd, Kd = O.widen(Q), O.widen(K)
+    L, n, Hq, dh = Qd.shape
+    scale = 1 / math.sqrt(dh) if scale is None else scale
+    out = np.full((L, Hq, n), -np.inf)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        for l in range(L):
+            for h in range(Hq):
+                s = scale * Qd[l, lo:hi, h] @ Kd[l, lo:hi, h // (Hq // Kd.shape[2])].T
+                s = np.where(np.arange(hi - lo)[None, :] < np.arange(hi - lo)[:, None], s, -np.inf)
+                m = s.max(axis=1)
+                with np.errstate(invalid="ignore"):
+                    out[l, h, lo:hi] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    return out
+
+
+def _head_mutant(kind):
+    def f(pooled, y, edges, centres, W1, b1, W2, b2, lambda3, act="relu"):
+        h = np.asarray(pooled, dtype=np.float64); y = np.asarray(y, dtype=np.float64)
+        c = np.asarray(centres, dtype=np.float64)
+        W1, b1, W2, b2 = (np.asarray(t, dtype=np.float64) for t in (W1, b1, W2, b2))
+        B, K = h.shape[0], W2.shape[0]
+        z = h @ W1.T + b1
+        a = O._act(z, act)
+        o = a @ W2.T + b2
+        lse = np.log(np.exp(o - o.max(axis=1, keepdims=True)).sum(axis=1, keepdims=True)) + o.max(axis=1, keepdims=True)
+        ph = np.exp(o - lse)
+        yh = ph @ c
+        bins = O.length_bin(y, edges)
+        if kind == "hard_labels":
+            p = np.eye(K)[bins]
+        else:
+            p = np.stack([O.soft_labels(int(i), K) for i in bins])
+        loss = O.length_loss(p, ph, y, yh, lambda3)
+        sgn = 2.0 if kind == "mse_grad_sign" else -2.0
+        do = lambda3 * (ph - p) + (1 - lambda3) * (sgn * (y - yh))[:, None] * ph * (c[None, :] - yh[:, None])
+        if kind != "no_batch_mean":
+            do = do / B
+        g = {"W2": do.T @ (z if kind == "w2_grad_from_z" else a), "b2": do.sum(axis=0)}
+        dz = (do @ W2) * O._act_grad(a if kind == "act_grad_of_output" else z, act)
+        g["W1"] = dz.T @ h
+        g["b1"] = dz.sum(axis=0)
+        return loss, g
+    return f
+
+
+def _adamw_mutant(kind):
+    def f(theta, grad, m, v, t, lr, beta1, beta2, eps, weight_decay):
+        theta = np.asarray(theta, dtype=np.float64)
+        g = grad + weight_decay * theta if kind == "coupled_decay" else grad
+        th = theta if kind == "coupled_decay" else theta * (1 - lr * weight_decay)
+        m = beta1 * np.asarray(m, dtype=np.float64) + (1 - beta1) * g
+        v = beta2 * np.asarray(v, dtype=np.float64) + (1 - beta2) * g * g
+        mh = m if kind == "no_bias_correction" else m / (1 - beta1 ** t)
+        vh = v if kind == "no_bias_correction" else v / (1 - beta2 ** t)
+        den = np.sqrt(vh + eps) if kind == "eps_inside_sqrt" else np.sqrt(vh) + eps
+        return th - lr * mh / den, m, v
+    return f
+
+
+def _misalignment_mutant(kind):
+    def f(H, S, cu, frac_low=0.4, frac_high=0.4):
+        out = np.zeros((len(cu) - 1, 4), dtype=np.int64)
+        for b in range(len(cu) - 1):
+            lo, hi = int(cu[b]), int(cu[b + 1])
+            sets = []
+            for v in (np.asarray(H, float)[lo:hi], np.asarray(S, float)[lo:hi]):
+                N = len(v)
+                if kind == "ties_by_higher_index":
+                    order = np.lexsort((-np.arange(N), v))
+                else:
+                    order = np.argsort(v, kind="stable")
+                rnd = math.ceil if kind == "ceil_counts" else math.floor
+                nl, nh = int(rnd(frac_low * N)), int(rnd(frac_high * N))
+                low = np.zeros(N, bool); high = np.zeros(N, bool)
+                low[order[:nl]] = True; high[order[N - nh:]] = True
+                sets.append((high, low) if kind == "low_high_swapped" else (low, high))
+            (lowH, highH), (lowS, highS) = sets
+            out[b] = [highH.sum(), (highH & lowS).sum(), lowH.sum(), (lowH & highS).sum()]
+        return out
+    return f
+
+
+def _sjf_jct_uses_max(lengths, order, batch):
+    y = np.asarray(lengths, dtype=np.int64)
+    order = np.arange(len(y)) if order is None else np.asarray(order)
+    padded = useful = jct = start = 0
+    for k0 in range(0, len(order), batch):
+        mem = y[order[k0:k0 + batch]]
+        mx = int(mem.max())
+        padded += len(mem) * mx - int(mem.sum()); useful += int(mem.sum())
+        jct += len(mem) * (start + mx)
+        start += mx
+    return padded, useful, jct
+
+
+LATER_MUTANTS = {
+    "row_lse_excludes_diagonal": ("attn_row_lse", _row_lse_excl_diag,
+                                  [P.test_row_lse_bruteforce, P.test_row_lse_closed_forms]),
+    "row_lse_ignores_scale": ("attn_row_lse", lambda Q, K, cu, scale=None, row_chunk=2048: O.attn_row_lse(Q, K, cu),
+                              [P.test_row_lse_bruteforce, P.test_row_lse_closed_forms]),
+    "from_lse_ignores_given_lse": ("attn_importance_from_lse",
+                                   lambda Q, K, cu, lse, scale=None, row_chunk=2048, exclude_self=False,
+                                   layer_weights=None: O.attn_importance(Q, K, cu, scale, exclude_self=exclude_self,
+                                                                         layer_weights=layer_weights),
+                                   [P.test_importance_from_lse_bruteforce_and_identity]),
+    "head_mse_grad_sign": ("head_loss_and_grads", _head_mutant("mse_grad_sign"),
+                           [lambda: P.test_head_gradients_match_finite_differences("relu")]),
+    "head_no_batch_mean": ("head_loss_and_grads", _head_mutant("no_batch_mean"),
+                           [lambda: P.test_head_gradients_match_finite_differences("relu")]),
+    "head_w2_grad_from_z": ("head_loss_and_grads", _head_mutant("w2_grad_from_z"),
+                            [lambda: P.test_head_gradients_match_finite_differences("gelu_tanh")]),
+    "head_act_grad_of_output": ("head_loss_and_grads", _head_mutant("act_grad_of_output"),
+                                [lambda: P.test_head_gradients_match_finite_differences("gelu_tanh")]),
+    "head_hard_labels": ("head_loss_and_grads", _head_mutant("hard_labels"),
+                         [P.test_head_loss_soft_labels_by_hand]),
+    "adamw_no_bias_correction": ("adamw_step", _adamw_mutant("no_bias_correction"), [P.test_adamw_closed_forms]),
+    "adamw_coupled_decay": ("adamw_step", _adamw_mutant("coupled_decay"), [P.test_adamw_closed_forms]),
+    "adamw_eps_inside_sqrt": ("adamw_step", _adamw_mutant("eps_inside_sqrt"), [P.test_adamw_closed_forms]),
+    "misalignment_ties_by_higher_index": ("misalignment_counts", _misalignment_mutant("ties_by_higher_index"),
+                                          [P.test_misalignment_by_hand, P.test_misalignment_bruteforce_ranks]),
+    "misalignment_ceil_counts": ("misalignment_counts", _misalignment_mutant("ceil_counts"),
+                                 [P.test_misalignment_by_hand, P.test_misalignment_bruteforce_ranks]),
+    "misalignment_low_high_swapped": ("misalignment_counts", _misalignment_mutant("low_high_swapped"),
+                                      [P.test_misalignment_by_hand, P.test_misalignment_bruteforce_ranks]),
+    "sjf_jct_uses_batch_max": ("sjf_padding", _sjf_jct_uses_max, [P.test_sjf_padding_by_hand]),
+}
+
+
+@pytest.mark.parametrize("name", list(LATER_MUTANTS))
+def test_later_mutant_caught(name, monkeypatch):
+    attr, fn, pins = LATER_MUTANTS[name]
+    monkeypatch.setattr(oracle, attr, fn)
+    caught = False
+    for pin in pins:
+        try:
+            with np.errstate(all="ignore"):
+                pin()
+        except Exception:
+            caught = True
+            break
+    assert caught, name
+
+
+def test_later_pins_pass_unmutated():
+    for _, _, pins in LATER_MUTANTS.values():
+        for pin in pins:
+            pin()

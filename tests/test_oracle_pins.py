@@ -687,3 +687,18 @@ def test_sjf_padding_by_hand():
     assert oracle.sjf_padding(y, [1, 3, 0, 2], 2) == (1 + 4, 17, (1 + 2) + (2 * 2 + 14))
     # a ragged last batch
     assert oracle.sjf_padding([3, 3, 3], None, 2) == (0, 9, (3 + 3) + (3 + 3))
+
+
+def test_head_loss_soft_labels_by_hand():
+    # a = act(0) = 0 so o = b2 = (0, ln 2, 0): p-hat = (1, 2, 1) / 4.  y = 5 sits in bin 0, so the
+    # Eq. 6 targets are (1, e^-1, e^-2) / (1 + e^-1 + e^-2); y-hat = p-hat . c
+    h = np.zeros((1, 3))
+    W1 = np.zeros((2, 3)); b1 = np.zeros(2); W2 = np.zeros((3, 2)); b2 = np.array([0.0, math.log(2.0), 0.0])
+    edges = np.array([0.0, 10.0, 20.0, 30.0]); c = np.array([5.0, 15.0, 25.0])
+    lam = 0.7
+    loss, _ = oracle.head_loss_and_grads(h, [5.0], edges, c, W1, b1, W2, b2, lam)
+    q = np.array([1.0, math.exp(-1.0), math.exp(-2.0)]); q /= q.sum()
+    ph = np.array([0.25, 0.5, 0.25])
+    ce = -(q * np.log(ph)).sum()
+    yhat = (ph * c).sum()
+    assert loss == pytest.approx(lam * ce + (1 - lam) * (5.0 - yhat) ** 2, rel=1e-14)
