@@ -66,25 +66,42 @@ def cpu_baseline(inp, lam1, lam2, alpha, norm, n_prompts: int):
     }
 
 
-def recorded_traffic(workload: str):
-    """HBM bytes per launch of the entropy kernel from the committed rocprofv3 counter summary,
-    or None when that summary is for another workload or for a different kernel source."""
+def _entropy_source_hash() -> str:
     import hashlib
-    import re
-    if workload != "llama":
-        return None
-    path = os.path.join(ROOT, "profiles", "llama_path_hbm_counters.md")
-    try:
-        txt = open(path).read()
-    except OSError:
-        return None
-    m = re.search(r"entropy_gemm traffic_bytes=(\d+) source_sha256_16=([0-9a-f]+)", txt)
-    if not m:
-        return None
     h = hashlib.sha256()
     for f in ("paper_2608_15592_amd/csrc/entropy.hip", "paper_2608_15592_amd/csrc/estp_common.h"):
         h.update(open(os.path.join(ROOT, f), "rb").read())
-    return float(m.group(1)) if h.hexdigest()[:16] == m.group(2) else None
+    return h.hexdigest()[:16]
+
+
+def _recorded_line(workload: str, fname: str, pattern: str):
+    """Fields of the machine-readable line of a committed rocprofv3 summary, or None when the
+    summary is for another workload or was taken on a different entropy-kernel source."""
+    import re
+    if workload != "llama":
+        return None
+    try:
+        txt = open(os.path.join(ROOT, "profiles", fname)).read()
+    except OSError:
+        return None
+    m = re.search(pattern + r" source_sha256_16=([0-9a-f]+)", txt)
+    if not m or m.group(m.lastindex) != _entropy_source_hash():
+        return None
+    return m.groups()[:-1]
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch of the entropy kernel (calibrated FETCH_SIZE + WRITE_SIZE)."""
+    g = _recorded_line(workload, "llama_path_hbm_counters.md", r"entropy_gemm traffic_bytes=(\d+)")
+    return float(g[0]) if g else None
+
+
+def recorded_clock(workload: str):
+    """(sustained core clock in GHz, matrix-pipe busy fraction) of the entropy kernel, from the
+    GRBM_GUI_ACTIVE / SQ_VALU_MFMA_BUSY_CYCLES counter summary."""
+    g = _recorded_line(workload, "entropy_gemm_llama_clock_mfma_busy.md",
+                       r"entropy_gemm sustained_clock_mhz=([0-9.]+) mfma_busy=([0-9.]+)")
+    return (float(g[0]) / 1000.0, float(g[1])) if g else None
 
 
 def row_lse_torch(Q, K, cu_seqlens, scale, torch, rows: int = 1024):
@@ -118,7 +135,7 @@ def main() -> int:
     ap.add_argument("--lambda1", type=float, default=0.5)
     ap.add_argument("--lambda2", type=float, default=0.5)
     ap.add_argument("--alpha", type=float, default=1.0)
-    ap.add_argument("--norm", default="none", choices=["none", "zscore"])
+    ap.add_argument("--norm", default="none", choices=["none", "zscore", "minmax"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-prompts", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -204,6 +221,7 @@ def main() -> int:
     ms_per_step = total_ms / args.steps
     per_call = np.array([[e[k].elapsed_time(e[k + 1]) for k in range(4)] for e in evs])
     ent_ms, imp_ms, pool_ms, pred_ms = per_call.mean(axis=0)
+    med_ms = np.median(per_call, axis=0)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step "
         f"(entropy {ent_ms:.3f}, importance {imp_ms:.3f}, combine+pool {pool_ms:.3f}, head {pred_ms:.3f} ms)")
 
@@ -271,11 +289,25 @@ def main() -> int:
                         "ordered by the predicted lengths, synthetic true lengths"}
     log(f"analyses: misalignment {analyses['misalignment_ms']:.3f} ms, sjf padding {analyses['sjf_padding_ms']:.3f} ms")
 
+    # A plain device-to-device copy of X, the bandwidth the pooling call is set against.
+    Xc = torch.empty_like(X)
+    Xc.copy_(X)
+    cp_evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for k in range(5):
+        cp_evs[k].record(stream)
+        Xc.copy_(X)
+    cp_evs[5].record(stream)
+    torch.cuda.synchronize()
+    copy_ms = float(np.median([cp_evs[k].elapsed_time(cp_evs[k + 1]) for k in range(5)]))
+    copy_gbps = 2 * X.numel() * X.element_size() / (copy_ms * 1e-3) / 1e9
+    del Xc
+
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
     pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
     ent_tflops = ent_flop / (ent_ms * 1e-3) / 1e12
     pool_gbps = pool_bytes / (pool_ms * 1e-3) / 1e9
+    clock = recorded_clock(args.workload)
     result = {
         "metric": METRIC,
         "value": n_tok / (ms_per_step * 1e-3),
@@ -304,9 +336,15 @@ def main() -> int:
             "frac": ent_tflops / PEAK_BF16_TFLOPS,
             "traffic": recorded_traffic(args.workload),
             "work_per_launch": f"2*n_tok*V*d = {ent_flop:.4g} FLOP",
+            # from the committed GRBM_GUI_ACTIVE / SQ_VALU_MFMA_BUSY_CYCLES summary of this kernel source
+            "sustained_clock_GHz": clock[0] if clock else None,
+            "frac_at_sustained_clock": ent_tflops / (PEAK_BF16_TFLOPS * clock[0] / 2.4) if clock else None,
+            "mfma_busy": clock[1] if clock else None,
         },
         "kernels_ms": {"token_entropy": ent_ms, "attn_importance": imp_ms, "combine_pool": pool_ms,
                        "predict": pred_ms},
+        "kernels_ms_median": dict(zip(("token_entropy", "attn_importance", "combine_pool", "predict"),
+                                      (float(v) for v in med_ms))),
         "importance": {"alg_flop": imp_flop_alg, "alg_tflops": imp_flop_alg / (imp_ms * 1e-3) / 1e12,
                        "executed_tflops": 2 * imp_flop_alg / (imp_ms * 1e-3) / 1e12},
         "importance_from_prefill_lse": {"ms": lse_ms, "vs_two_pass": lse_ms / imp_ms,
@@ -318,7 +356,10 @@ def main() -> int:
         "analyses": analyses,
         "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
                     "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
-                    "note": "whole combine_pool call (weights + pooling + chunk reduction), warm after importance"},
+                    "device_copy_GBps": copy_gbps, "frac_of_device_copy": pool_gbps / copy_gbps,
+                    "note": "whole combine_pool call (weights + pooling + chunk reduction); X is not cache "
+                            "resident (importance streams 2.7 GB of Q and K just before); device copy counts "
+                            "read + write bytes"},
         "device": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:

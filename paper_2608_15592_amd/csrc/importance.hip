@@ -13,7 +13,7 @@
 //
 // Pass 2 (attn_colsum_kernel): one workgroup per (layer, KV head, prompt,
 // 256-key block); each wave keeps 64 keys as B fragments in registers and
-// streams, through LDS, every later 32-query block of every query head that
+// streams, through LDS, every later 64-query block of every query head that
 // shares the KV head (grouped-query reuse: the keys are read once).  Scores
 // are formed as S = Q K^T, so a lane owns one key column and 16 query rows of
 // each 32 x 32 block; 2^(c s - lse2) is summed per lane into column sums.
@@ -33,7 +33,8 @@ constexpr int kQBlock = 4 * kQPerWave;
 constexpr int kKPerWave = 64;  // keys per wave in pass 2
 constexpr int kKBlock = 4 * kKPerWave;
 constexpr int kKTile = 64;     // keys per streamed tile in pass 1
-constexpr int kQTile = 32;     // queries per streamed tile in pass 2 (64 spills or costs a wave)
+constexpr int kQTile = 64;     // queries per streamed tile in pass 2 (two 32-query row blocks in turn)
+static_assert(kKBlock % kQTile == 0 && kQTile % 32 == 0, "pass-2 tiles must tile a key block");
 
 // Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
 // consecutive rows read at one logical chunk hit 16 distinct bank groups.
@@ -274,30 +275,27 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
     const int i0 = qb * kQTile;
     if (i0 + kQTile - 1 >= k0 && k0 < N) {  // some query of the tile sees some key of this wave
       const char* qt = qtile[t & 1];
-      constexpr int kRB = kQTile / 32;  // 32-query row blocks per tile
-      f32x16_t acc[kRB][2];
-#pragma unroll
-      for (int rb = 0; rb < kRB; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(rb * 32 + col, ks * 2 + half));
-#pragma unroll
-          for (int cb = 0; cb < 2; ++cb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[rb][cb], 0, 0, 0);
-        }
-      }
-      // acc[rb][cb][r]: query i0 + rb*32 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
       const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
       // tiles holding some query i <= (or, strict, ==) a key of this wave need the mask
       const bool diag = i0 < k0 + kKPerWave - 1 + strict;
+      // The tile's 32-query row blocks go one after another through the same
+      // accumulators: the tile, and so the barrier, is twice as long as one
+      // 32 x 64 block of scores without a second set of registers.
 #pragma unroll
-      for (int rb = 0; rb < kRB; ++rb) {
+      for (int rb = 0; rb < kQTile / 32; ++rb) {
+        f32x16_t acc[2];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(rb * 32 + col, ks * 2 + half));
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+            acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[cb], 0, 0, 0);
+        }
+        // acc[cb][r]: query i0 + rb*32 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
         float lr[16];
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
@@ -315,12 +313,12 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
               const int i = i0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-              const float p = fast_exp2(fmaf(acc[rb][cb][r], c2, -lr[r]));
+              const float p = fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
               cs += (j < i + 1 - strict) ? p : 0.f;
             }
           } else {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) cs += fast_exp2(fmaf(acc[rb][cb][r], c2, -lr[r]));
+            for (int r = 0; r < 16; ++r) cs += fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
           }
           csum[cb] += cs;
         }

@@ -24,6 +24,7 @@ constexpr int kChunk = 256;                // rows per pooling workgroup (= thre
 constexpr int kSlice = kThreads * 8;       // hidden features per pooling workgroup
 constexpr float kZEps = 1e-6f;
 constexpr int kMaxChunks = 1024;           // chunks per prompt the finisher stages (prompts up to 256k tokens)
+constexpr int kFinishBatch = 8;            // chunk partials the finisher loads at once
 
 struct ChunkStat {
   float m;    // max of u over the chunk
@@ -267,7 +268,10 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
 // Combine the chunks of prompt b in a fixed order:
 // pooled = sum_c 2^((m_c - M) log2 e) partial_c / Z,  Z = sum_c 2^((m_c - M) log2 e) s_c.
 // Workgroups x < nslices each finish a 2048-feature slice; the rest write the
-// normalised weights e of 1024 tokens each (when asked); x = 0 writes the top token.
+// normalised weights e of kThreads tokens each (when asked); x = 0 writes the
+// top token.  Every load that does not need the chunk statistics (the token's
+// S and H, the first kFinishBatch chunk partials) is issued before them, so the
+// kernel costs about two memory round trips.
 __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __restrict__ part,
                                                                const ChunkStat* __restrict__ cstat,
                                                                const float* __restrict__ S,
@@ -283,6 +287,29 @@ __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __re
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   const int nch = (N + kChunk - 1) / kChunk;
+  const bool weights = slice >= nslices;
+  if (weights && !e) return;
+  const int wi = (slice - nslices) * kThreads + threadIdx.x;  // weights slice: this thread's token
+  float sv = 0.f, hv = 0.f;
+  if (weights && wi < N) {
+    sv = S[base + wi];
+    hv = H[base + wi];
+  }
+  const int c = (slice * kThreads + threadIdx.x) * 8;  // pooling slice: this thread's 8 features
+  const bool pool = !weights && c < d;
+  const float* p = part + size_t(b) * n_chunk_max * d + c;
+  float4 x[2 * kFinishBatch];
+  auto load_batch = [&](int k) {
+#pragma unroll
+    for (int j = 0; j < kFinishBatch; ++j) {
+      if (k + j < nch) {
+        x[2 * j] = *reinterpret_cast<const float4*>(p + size_t(k + j) * d);
+        x[2 * j + 1] = *reinterpret_cast<const float4*>(p + size_t(k + j) * d + 4);
+      }
+    }
+  };
+  if (pool) load_batch(0);
+
   for (int k = threadIdx.x; k < nch; k += kThreads) cs[k] = cstat[size_t(b) * n_chunk_max + k];
   __syncthreads();
   float M = -INFINITY;
@@ -296,33 +323,34 @@ __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __re
   for (int k = 0; k < nch; ++k) Z += cs[k].s * fast_exp2((cs[k].m - M) * kLog2e);
   const float invZ = 1.f / Z;
 
-  if (slice >= nslices) {  // weights of tokens [1024 (slice - nslices), + 1024)
-    if (!e) return;
-    const float4 cf = coef_of(coef, b, a1, a2);
-    const int i1 = min(N, (slice - nslices + 1) * 1024);
-    for (int i = (slice - nslices) * 1024 + threadIdx.x; i < i1; i += kThreads) {
-      const float u = fmaf(cf.x, S[base + i], fmaf(cf.y, H[base + i], cf.z));
-      e[base + i] = fast_exp2((u - M) * kLog2e) * invZ;
+  if (weights) {
+    if (wi < N) {
+      const float4 cf = coef_of(coef, b, a1, a2);
+      const float u = fmaf(cf.x, sv, fmaf(cf.y, hv, cf.z));
+      e[base + wi] = fast_exp2((u - M) * kLog2e) * invZ;
     }
     return;
   }
   if (slice == 0 && top && threadIdx.x == 0) top[b] = base + Mi;
-  const int c = (slice * kThreads + threadIdx.x) * 8;
-  if (c < d) {
+  if (pool) {
+    // chunks summed in ascending order, kFinishBatch partials in flight at a time
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const float* p = part + size_t(b) * n_chunk_max * d + c;
-    for (int k = 0; k < nch; ++k) {
-      const float w = fast_exp2((cs[k].m - M) * kLog2e) * invZ;
-      const float4 x0 = *reinterpret_cast<const float4*>(p + size_t(k) * d);
-      const float4 x1 = *reinterpret_cast<const float4*>(p + size_t(k) * d + 4);
-      acc[0] = fmaf(w, x0.x, acc[0]);
-      acc[1] = fmaf(w, x0.y, acc[1]);
-      acc[2] = fmaf(w, x0.z, acc[2]);
-      acc[3] = fmaf(w, x0.w, acc[3]);
-      acc[4] = fmaf(w, x1.x, acc[4]);
-      acc[5] = fmaf(w, x1.y, acc[5]);
-      acc[6] = fmaf(w, x1.z, acc[6]);
-      acc[7] = fmaf(w, x1.w, acc[7]);
+    for (int k = 0; k < nch; k += kFinishBatch) {
+      if (k > 0) load_batch(k);
+#pragma unroll
+      for (int j = 0; j < kFinishBatch; ++j) {
+        if (k + j < nch) {
+          const float w = fast_exp2((cs[k + j].m - M) * kLog2e) * invZ;
+          acc[0] = fmaf(w, x[2 * j].x, acc[0]);
+          acc[1] = fmaf(w, x[2 * j].y, acc[1]);
+          acc[2] = fmaf(w, x[2 * j].z, acc[2]);
+          acc[3] = fmaf(w, x[2 * j].w, acc[3]);
+          acc[4] = fmaf(w, x[2 * j + 1].x, acc[4]);
+          acc[5] = fmaf(w, x[2 * j + 1].y, acc[5]);
+          acc[6] = fmaf(w, x[2 * j + 1].z, acc[6]);
+          acc[7] = fmaf(w, x[2 * j + 1].w, acc[7]);
+        }
+      }
     }
     float* out = pooled + size_t(b) * d + c;
     *reinterpret_cast<float4*>(out) = make_float4(acc[0], acc[1], acc[2], acc[3]);
@@ -405,7 +433,7 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
                                                                nch, a1, a2, cf, part, cstat);
   }
   ESTP_CHECK_LAUNCH("pool_partial_kernel");
-  const int ne = e ? (max_seqlen + 1023) / 1024 : 0;
+  const int ne = e ? (max_seqlen + kThreads - 1) / kThreads : 0;
   pool_finish_kernel<<<dim3(nslices + ne, B), dim3(kThreads), 0, s>>>(part, cstat, S, H, cu_seqlens, int(d), nch,
                                                                       nslices, a1, a2, cf, pooled, e, top);
   ESTP_CHECK_LAUNCH("pool_finish_kernel");
