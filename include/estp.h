@@ -97,7 +97,9 @@ ESTP_API const char* estp_last_error(void);
  *   W  [V, d]      LM-head weight in nn.Linear layout (dtype), 16-byte aligned
  *   H  [n_tok]     float32 output
  *   dtype          ESTP_BF16 (ESTP_F32 returns ESTP_ERR_UNSUPPORTED)
- * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0.
+ * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0; a d that is not a
+ * multiple of 32 returns ESTP_ERR_UNSUPPORTED (the matrix-core k steps are
+ * 16 deep and a stage row is at least 64 bytes).
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype);
 ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
@@ -197,7 +199,8 @@ ESTP_API int estp_attn_importance_ex(const void* Q, const void* K, const float* 
  *   top [B]          int32 output: global index of each prompt's largest
  *                    weight (lowest index among equal maxima), or NULL
  *   dtype            ESTP_BF16 or ESTP_F32
- * Requires d >= 8, d % 8 == 0.
+ * Requires d >= 8, d % 8 == 0.  A prompt longer than 262144 tokens returns
+ * ESTP_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d, int dtype);
 ESTP_API int estp_combine_pool(const void* X, const float* S, const float* H, const int32_t* cu_seqlens, int32_t B,

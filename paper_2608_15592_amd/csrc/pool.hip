@@ -14,6 +14,8 @@
 // per-prompt statistics pass (zscore_stats_kernel, minmax_stats_kernel) runs
 // first and folds the scaling into u = a1 S + a2 H + c0.  No atomics: results
 // are bitwise reproducible.
+#include <algorithm>
+
 #include "estp_common.h"
 
 namespace estp {
@@ -186,17 +188,34 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
                                                                 const int* __restrict__ cu, int d, int n_chunk_max,
                                                                 float a1, float a2, const float4* __restrict__ coef,
                                                                 float* __restrict__ part,
-                                                                ChunkStat* __restrict__ cstat) {
+                                                                ChunkStat* __restrict__ cstat, int nslices,
+                                                                const int2* __restrict__ chunk_map) {
   __shared__ float wts[kThreads / 64][kChunk];  // one private copy of the chunk weights per wave
-  const int chunk = blockIdx.x;
-  const int b = blockIdx.y;
+  // One workgroup per (chunk, feature slice), slice fastest: the slices of a
+  // chunk (the two halves of its 8 KB rows at d = 4096) run together.  The
+  // chunk is (prompt, chunk) = (k / n_chunk_max, k % n_chunk_max), or, when
+  // many prompts are much shorter than the longest, the k-th entry of the
+  // list of live chunks (a grid sized by the longest prompt would be mostly
+  // workgroups that exit at once, and those cost ~25 ns each).
+  const int slice = blockIdx.x % nslices;
+  const int k = blockIdx.x / nslices;
+  int b, chunk;
+  if (chunk_map) {
+    const int2 bc = chunk_map[k];
+    if (bc.x < 0) return;  // past the live chunks
+    b = bc.x;
+    chunk = bc.y;
+  } else {
+    b = k / n_chunk_max;
+    chunk = k % n_chunk_max;
+  }
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   const int r0 = chunk * kChunk;
   if (r0 >= N) return;
   const int nr = min(N - r0, kChunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = (blockIdx.z * kThreads + threadIdx.x) * 8;
+  const int c = (slice * kThreads + threadIdx.x) * 8;
   const bool active = c < d;
   const T* xp = X + size_t(base + r0) * d + (active ? c : 0);
 
@@ -244,7 +263,7 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
     sc += p;
   }
   sc = wave_sum(sc);
-  if (threadIdx.x == 0 && blockIdx.z == 0) cstat[size_t(b) * n_chunk_max + chunk] = ChunkStat{m, sc, mi, 0};
+  if (threadIdx.x == 0 && slice == 0) cstat[size_t(b) * n_chunk_max + chunk] = ChunkStat{m, sc, mi, 0};
 
   if (!active) return;
   const float* w = wts[wave];
@@ -265,6 +284,40 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
   *reinterpret_cast<float4*>(out + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
 }
 
+// List of live chunks: entry k = (prompt, chunk) in prompt order, then
+// (-1, 0) up to n_bound.  One workgroup: each thread counts the chunks of a
+// run of consecutive prompts, an exclusive scan over the threads places them.
+// Counts are capped at n_chunk_max and writes at n_bound, so a max_seqlen below
+// the longest prompt (invalid input) stays inside the workspace.
+__global__ __launch_bounds__(1024) void chunk_map_kernel(const int* __restrict__ cu, int B, int n_chunk_max,
+                                                         int n_bound, int2* __restrict__ map) {
+  __shared__ int wsum[16];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int per = (B + 1023) / 1024;
+  const int b0 = min(B, t * per), b1 = min(B, b0 + per);
+  int cnt = 0;
+  for (int b = b0; b < b1; ++b) cnt += min((cu[b + 1] - cu[b] + kChunk - 1) / kChunk, n_chunk_max);
+  // inclusive scan within the wave, then over the 16 wave totals
+  int x = cnt;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int i = 0; i < 16; ++i) {
+    before += (i < w) ? wsum[i] : 0;
+    total += wsum[i];
+  }
+  int k = before + x - cnt;  // exclusive prefix: this thread's first entry
+  for (int b = b0; b < b1; ++b) {
+    const int nc = min((cu[b + 1] - cu[b] + kChunk - 1) / kChunk, n_chunk_max);
+    for (int c = 0; c < nc && k < n_bound; ++c) map[k++] = make_int2(b, c);
+  }
+  for (int i = total + t; i < n_bound; i += 1024) map[i] = make_int2(-1, 0);
+}
+
 // Combine the chunks of prompt b in a fixed order:
 // pooled = sum_c 2^((m_c - M) log2 e) partial_c / Z,  Z = sum_c 2^((m_c - M) log2 e) s_c.
 // Workgroups x < nslices each finish a 2048-feature slice; the rest write the
@@ -277,16 +330,16 @@ __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __re
                                                                const float* __restrict__ S,
                                                                const float* __restrict__ H,
                                                                const int* __restrict__ cu, int d, int n_chunk_max,
-                                                               int nslices, float a1, float a2,
+                                                               int nslices, int n_finish, float a1, float a2,
                                                                const float4* __restrict__ coef,
                                                                float* __restrict__ pooled, float* __restrict__ e,
                                                                int* __restrict__ top) {
   __shared__ ChunkStat cs[kMaxChunks];
-  const int slice = blockIdx.x;
-  const int b = blockIdx.y;
+  const int slice = blockIdx.x % n_finish;  // n_finish workgroups per prompt
+  const int b = blockIdx.x / n_finish;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
-  const int nch = (N + kChunk - 1) / kChunk;
+  const int nch = min((N + kChunk - 1) / kChunk, n_chunk_max);
   const bool weights = slice >= nslices;
   if (weights && !e) return;
   const int wi = (slice - nslices) * kThreads + threadIdx.x;  // weights slice: this thread's token
@@ -364,6 +417,14 @@ __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __re
 using namespace estp;
 using namespace estp::detail;
 
+namespace {
+// Upper bound on the chunks that hold tokens: sum_b ceil(N_b / kChunk) <= n_tok / kChunk + B.
+size_t live_chunk_bound(int64_t n_tok, int32_t B, int32_t max_seqlen) {
+  const size_t nch = (size_t(max_seqlen) + kChunk - 1) / kChunk;
+  return std::min(size_t(B) * nch, size_t(n_tok) / kChunk + size_t(B));
+}
+}  // namespace
+
 extern "C" size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d,
                                                    int dtype) {
   (void)dtype;
@@ -373,6 +434,7 @@ extern "C" size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int
   c.take<float4>(size_t(B));            // per-prompt coefficients (z-score)
   c.take<ChunkStat>(size_t(B) * nch);   // chunk statistics
   c.take<float>(size_t(B) * nch * d);   // chunk partials
+  c.take<int2>(live_chunk_bound(n_tok, B, max_seqlen));  // list of live chunks
   return c.bytes();
 }
 
@@ -408,10 +470,19 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
 
   const int nch = (max_seqlen + kChunk - 1) / kChunk;
   const int nslices = (d + kSlice - 1) / kSlice;
+  // the full (prompt, chunk) grid, or the list of live chunks when that is clearly shorter
+  const size_t n_bound = live_chunk_bound(n_tok, B, max_seqlen);
+  const bool use_map = n_bound * 4 < size_t(B) * nch * 3;
+  const size_t n_k = use_map ? n_bound : size_t(B) * nch;
+  const int ne = e ? (max_seqlen + kThreads - 1) / kThreads : 0;
+  const int n_finish = nslices + ne;
+  ESTP_REQUIRE(n_k * nslices <= INT32_MAX && size_t(n_finish) * B <= INT32_MAX, ESTP_ERR_UNSUPPORTED,
+               "estp_combine_pool: batch too large for one launch");
   Carver c(workspace);
   float4* coef = c.take<float4>(size_t(B));
   ChunkStat* cstat = c.take<ChunkStat>(size_t(B) * nch);
   float* part = c.take<float>(size_t(B) * nch * d);
+  int2* map = c.take<int2>(n_bound);
   const float a1 = lambda1 / alpha, a2 = lambda2 / alpha;
   const float4* cf = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -424,18 +495,22 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
     ESTP_CHECK_LAUNCH("minmax_stats_kernel");
     cf = coef;
   }
-  const dim3 grid(nch, B, nslices);
+  if (use_map) {
+    chunk_map_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu_seqlens, B, nch, int(n_bound), map);
+    ESTP_CHECK_LAUNCH("chunk_map_kernel");
+  }
+  const dim3 grid(unsigned(n_k * nslices));
+  const int2* cmap = use_map ? map : nullptr;
   if (dtype == ESTP_BF16) {
     pool_partial_kernel<uint16_t><<<grid, dim3(kThreads), 0, s>>>(static_cast<const uint16_t*>(X), S, H, cu_seqlens,
-                                                                  int(d), nch, a1, a2, cf, part, cstat);
+                                                                  int(d), nch, a1, a2, cf, part, cstat, nslices, cmap);
   } else {
     pool_partial_kernel<float><<<grid, dim3(kThreads), 0, s>>>(static_cast<const float*>(X), S, H, cu_seqlens, int(d),
-                                                               nch, a1, a2, cf, part, cstat);
+                                                               nch, a1, a2, cf, part, cstat, nslices, cmap);
   }
   ESTP_CHECK_LAUNCH("pool_partial_kernel");
-  const int ne = e ? (max_seqlen + kThreads - 1) / kThreads : 0;
-  pool_finish_kernel<<<dim3(nslices + ne, B), dim3(kThreads), 0, s>>>(part, cstat, S, H, cu_seqlens, int(d), nch,
-                                                                      nslices, a1, a2, cf, pooled, e, top);
+  pool_finish_kernel<<<dim3(unsigned(size_t(n_finish) * B)), dim3(kThreads), 0, s>>>(
+      part, cstat, S, H, cu_seqlens, int(d), nch, nslices, n_finish, a1, a2, cf, pooled, e, top);
   ESTP_CHECK_LAUNCH("pool_finish_kernel");
   return ESTP_OK;
 }

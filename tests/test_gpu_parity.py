@@ -257,6 +257,28 @@ def test_combine_pool_slices_and_reused_workspace():
             check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
 
 
+def test_combine_pool_many_short_prompts():
+    # one long prompt and 299 short ones: the pooling runs over the list of live chunks
+    # (the full prompt x chunk grid would be mostly empty), built by a scan over prompts
+    g = np.random.default_rng(11)
+    lengths = [2000] + g.integers(1, 41, size=299).tolist()
+    n = sum(lengths)
+    d = 4096
+    X = _bf16(g.standard_normal((n, d)).astype(np.float32))
+    S = (g.random(n) / 20).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    pooled, e, top = estp.combine_pool(dev(X), dev(S), dev(Hh), dev(cu), max(lengths), 0.6, 0.4, 1.0, "zscore")
+    e_ref, _ = oracle.combine_weights(S, Hh, cu, 0.6, 0.4, 1.0, "zscore")
+    p_ref = oracle.pool(X, e_ref, cu)
+    np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+    P, top = host(pooled), host(top)
+    for b in range(len(lengths)):
+        assert rel_l2(P[b], p_ref[b]) <= POOL_RTOL
+        lo, hi = cu[b], cu[b + 1]
+        check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
+
+
 # ------------------------------------------------------------------------------------------ length head
 
 @pytest.mark.parametrize("K,act,B,d,Hdn", [(1, "relu", 37, 256, 96), (8, "relu", 37, 256, 96),
