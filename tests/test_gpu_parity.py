@@ -55,6 +55,10 @@ ENTROPY_CASES = [
     (77, 32, 1300, 0.02, "width-32"),
     (300, 96, 2500, 0.02, "width-96-ragged"),
     (130, 4128, 3000, 0.02, "width-4128"),
+    # tile edges: one vocabulary row, exactly one 256 x 256 tile, one past it
+    (5, 64, 1, 0.02, "one-word-vocab"),
+    (256, 64, 256, 0.02, "exact-tile"),
+    (257, 64, 257, 0.02, "tile-plus-one"),
 ]
 
 
@@ -69,6 +73,22 @@ def test_entropy_parity(n_tok, d, V, std, tag):
     assert err <= H_TOL
     if std == 0.0:
         np.testing.assert_allclose(H, math.log(V), atol=H_TOL)
+
+
+def test_entropy_late_peak():
+    # weight rows scaled up along the vocabulary: the first tiles hold only small logits, so
+    # later tiles exceed the running reference by far more than 2^64 in weight and are
+    # refolded exactly with their own max (the ragged last tile always is)
+    n_tok, d, V = 300, 256, 12000
+    X = _hidden(n_tok, d, 5)
+    step = np.where(np.arange(V) < 7000, 0.05, 80.0).astype(np.float32)[:, None]
+    W = _bf16(np.random.default_rng(6).standard_normal((V, d)).astype(np.float32) * 0.02 * step)
+    H = host(estp.token_entropy(dev(X), dev(W)))
+    ref = oracle.token_entropy(X, W)
+    logits = oracle.widen(X)[:4] @ oracle.widen(W).T
+    print(f"late peak: logit range of the first tile {np.abs(logits[:, :256]).max():.1f}, "
+          f"overall {np.abs(logits).max():.1f}; max |dH| = {np.abs(H - ref).max():.3e}")
+    assert np.abs(H - ref).max() <= H_TOL
 
 
 def test_entropy_repeatable_bitwise():
