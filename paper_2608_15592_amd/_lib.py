@@ -126,9 +126,9 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream) -> ctypes.c_void_p:
+def _stream(stream, device=None) -> ctypes.c_void_p:
     if stream is None:
-        stream = torch.cuda.current_stream()
+        stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream)
 
 
@@ -145,7 +145,16 @@ def _need(t: torch.Tensor, name: str, device=None, dtype=None, ndim=None):
         raise ValueError(f"{name} is on {t.device}, expected {device}")
 
 
+def _sized(t: torch.Tensor, name: str, n: int, device=None, dtype=None):
+    """A device tensor of exactly n elements (contiguous, on ``device``, of ``dtype``)."""
+    _need(t, name, device=device, dtype=dtype)
+    if t.numel() != n:
+        raise ValueError(f"{name} must hold {n} elements, got {t.numel()}")
+
+
 def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    if workspace is not None:
+        _need(workspace, "workspace", device=device)
     if nbytes == 0:
         return workspace, 0
     if workspace is None:
@@ -176,8 +185,9 @@ def token_entropy(X: torch.Tensor, W: torch.Tensor, H: Optional[torch.Tensor] = 
         raise ValueError("H must have n_tok elements")
     dt = _dtype_code(X)
     workspace, wsb = _workspace(lib.estp_token_entropy_workspace_size(n_tok, d, V, dt), X.device, workspace)
-    _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(workspace), wsb,
-                                  _stream(stream)), "estp_token_entropy")
+    with torch.cuda.device(X.device):
+        _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(workspace), wsb,
+                                      _stream(stream, X.device)), "estp_token_entropy")
     return H
 
 
@@ -203,13 +213,14 @@ def attn_importance(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, 
         scale = 1.0 / math.sqrt(dh)
     if S is None:
         S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _need(S, "S", device=Q.device, dtype=torch.float32)
+    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
     ws = lib.estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
     workspace, wsb = _workspace(ws, Q.device, workspace)
-    _check(lib.estp_attn_importance(_ptr(Q), _ptr(K), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L, Hq, Hkv, dh,
-                                    float(scale), dt, _ptr(S), _ptr(workspace), wsb, _stream(stream)),
-           "estp_attn_importance")
+    with torch.cuda.device(Q.device):
+        _check(lib.estp_attn_importance(_ptr(Q), _ptr(K), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L, Hq, Hkv, dh,
+                                        float(scale), dt, _ptr(S), _ptr(workspace), wsb, _stream(stream, Q.device)),
+               "estp_attn_importance")
     return S
 
 
@@ -240,14 +251,15 @@ def attn_importance_from_lse(Q: torch.Tensor, K: torch.Tensor, lse: torch.Tensor
         scale = 1.0 / math.sqrt(dh)
     if S is None:
         S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _need(S, "S", device=Q.device, dtype=torch.float32)
+    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
     ws = lib.estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
     workspace, wsb = _workspace(ws, Q.device, workspace)
-    _check(lib.estp_attn_importance_from_lse(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok,
-                                             L, Hq, Hkv, dh, float(scale), dt, _ptr(S), _ptr(workspace), wsb,
-                                             _stream(stream)),
-           "estp_attn_importance_from_lse")
+    with torch.cuda.device(Q.device):
+        _check(lib.estp_attn_importance_from_lse(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen),
+                                                 n_tok, L, Hq, Hkv, dh, float(scale), dt, _ptr(S), _ptr(workspace),
+                                                 wsb, _stream(stream, Q.device)),
+               "estp_attn_importance_from_lse")
     return S
 
 
@@ -284,15 +296,16 @@ def attn_importance_ex(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tenso
         scale = 1.0 / math.sqrt(dh)
     if S is None:
         S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _need(S, "S", device=Q.device, dtype=torch.float32)
+    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
     ws = lib.estp_attn_importance_ex_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt, int(lse is not None))
     workspace, wsb = _workspace(ws, Q.device, workspace)
     flags = ESTP_IMPORTANCE_EXCLUDE_SELF if exclude_self else 0
-    _check(lib.estp_attn_importance_ex(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L,
-                                       Hq, Hkv, dh, float(scale), lw, flags, dt, _ptr(S), _ptr(workspace), wsb,
-                                       _stream(stream)),
-           "estp_attn_importance_ex")
+    with torch.cuda.device(Q.device):
+        _check(lib.estp_attn_importance_ex(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L,
+                                           Hq, Hkv, dh, float(scale), lw, flags, dt, _ptr(S), _ptr(workspace), wsb,
+                                           _stream(stream, Q.device)),
+               "estp_attn_importance_ex")
     return S
 
 
@@ -307,23 +320,30 @@ def combine_pool(X: torch.Tensor, S: torch.Tensor, H: torch.Tensor, cu_seqlens: 
     """
     lib = load()
     _need(X, "X", ndim=2)
-    _need(S, "S", device=X.device, dtype=torch.float32)
-    _need(H, "H", device=X.device, dtype=torch.float32)
-    _need(cu_seqlens, "cu_seqlens", device=X.device, dtype=torch.int32, ndim=1)
     n_tok, d = X.shape
+    _sized(S, "S", n_tok, device=X.device, dtype=torch.float32)
+    _sized(H, "H", n_tok, device=X.device, dtype=torch.float32)
+    _need(cu_seqlens, "cu_seqlens", device=X.device, dtype=torch.int32, ndim=1)
     B = cu_seqlens.numel() - 1
     if pooled is None:
         pooled = torch.empty(B, d, dtype=torch.float32, device=X.device)
+    _sized(pooled, "pooled", B * d, device=X.device, dtype=torch.float32)
     if e is None and want_e:
         e = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+    if e is not None:
+        _sized(e, "e", n_tok, device=X.device, dtype=torch.float32)
     if top is None and want_top:
         top = torch.empty(B, dtype=torch.int32, device=X.device)
+    if top is not None:
+        _sized(top, "top", B, device=X.device, dtype=torch.int32)
     dt = _dtype_code(X)
     workspace, wsb = _workspace(lib.estp_combine_pool_workspace_size(n_tok, B, max_seqlen, d, dt), X.device,
                                 workspace)
-    _check(lib.estp_combine_pool(_ptr(X), _ptr(S), _ptr(H), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, d,
-                                 float(lambda1), float(lambda2), float(alpha), NORMS[norm], dt, _ptr(pooled), _ptr(e),
-                                 _ptr(top), _ptr(workspace), wsb, _stream(stream)), "estp_combine_pool")
+    with torch.cuda.device(X.device):
+        _check(lib.estp_combine_pool(_ptr(X), _ptr(S), _ptr(H), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, d,
+                                     float(lambda1), float(lambda2), float(alpha), NORMS[norm], dt, _ptr(pooled),
+                                     _ptr(e), _ptr(top), _ptr(workspace), wsb, _stream(stream, X.device)),
+               "estp_combine_pool")
     return pooled, e, top
 
 
@@ -339,13 +359,17 @@ def predict(pooled: torch.Tensor, W1: torch.Tensor, b1: Optional[torch.Tensor], 
     Hd, K = W1.shape[0], W2.shape[0]
     if W1.shape[1] != d or W2.shape[1] != Hd:
         raise ValueError("head weight shapes disagree")
+    for t, n, size in ((b1, "b1", Hd), (b2, "b2", K), (centres, "centres", K)):
+        if t is not None:
+            _sized(t, n, size, device=pooled.device, dtype=torch.float32)
     yhat = torch.empty(B, dtype=torch.float32, device=pooled.device)
     bins = torch.empty(B, dtype=torch.int32, device=pooled.device) if K > 1 else None
     order = torch.empty(B, dtype=torch.int32, device=pooled.device) if want_order else None
     workspace, wsb = _workspace(lib.estp_predict_workspace_size(B, d, Hd, K), pooled.device, workspace)
-    _check(lib.estp_predict(_ptr(pooled), B, d, _ptr(W1), _ptr(b1), Hd, ACTS[act], _ptr(W2), _ptr(b2), K,
-                            _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb,
-                            _stream(stream)), "estp_predict")
+    with torch.cuda.device(pooled.device):
+        _check(lib.estp_predict(_ptr(pooled), B, d, _ptr(W1), _ptr(b1), Hd, ACTS[act], _ptr(W2), _ptr(b2), K,
+                                _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb,
+                                _stream(stream, pooled.device)), "estp_predict")
     return yhat, bins, order
 
 
@@ -380,12 +404,14 @@ def head_train_step(pooled: torch.Tensor, y: torch.Tensor, edges: torch.Tensor, 
         raise ValueError(f"theta, m, v must hold {n} values")
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=dev_)
+    _sized(loss, "loss", 1, device=dev_, dtype=torch.float32)
     workspace, wsb = _workspace(lib.estp_head_train_step_workspace_size(B, d, hidden, K), dev_, workspace)
-    _check(lib.estp_head_train_step(_ptr(pooled), _ptr(y), B, d, hidden, K, ACTS[act], _ptr(edges), _ptr(centres),
-                                    _ptr(theta), _ptr(m), _ptr(v), int(step), float(lambda3), float(lr),
-                                    float(beta1), float(beta2), float(eps), float(weight_decay), _ptr(loss),
-                                    _ptr(workspace), wsb, _stream(stream)),
-           "estp_head_train_step")
+    with torch.cuda.device(dev_):
+        _check(lib.estp_head_train_step(_ptr(pooled), _ptr(y), B, d, hidden, K, ACTS[act], _ptr(edges), _ptr(centres),
+                                        _ptr(theta), _ptr(m), _ptr(v), int(step), float(lambda3), float(lr),
+                                        float(beta1), float(beta2), float(eps), float(weight_decay), _ptr(loss),
+                                        _ptr(workspace), wsb, _stream(stream, dev_)),
+               "estp_head_train_step")
     return loss
 
 
@@ -395,12 +421,13 @@ def misalignment(H: torch.Tensor, S: torch.Tensor, cu_seqlens: torch.Tensor, fra
     #high-H that are low-S, #low-H, #low-H that are high-S."""
     lib = load()
     _need(H, "H", dtype=torch.float32, ndim=1)
-    _need(S, "S", device=H.device, dtype=torch.float32, ndim=1)
+    _sized(S, "S", H.numel(), device=H.device, dtype=torch.float32)
     _need(cu_seqlens, "cu_seqlens", device=H.device, dtype=torch.int32, ndim=1)
     B = cu_seqlens.numel() - 1
     counts = torch.empty(B, 4, dtype=torch.int32, device=H.device)
-    _check(lib.estp_misalignment(_ptr(H), _ptr(S), _ptr(cu_seqlens), B, float(frac_low), float(frac_high),
-                                 _ptr(counts), _stream(stream)), "estp_misalignment")
+    with torch.cuda.device(H.device):
+        _check(lib.estp_misalignment(_ptr(H), _ptr(S), _ptr(cu_seqlens), B, float(frac_low), float(frac_high),
+                                     _ptr(counts), _stream(stream, H.device)), "estp_misalignment")
     return counts
 
 
@@ -409,8 +436,10 @@ def sjf_padding(lengths: torch.Tensor, order: Optional[torch.Tensor], batch: int
     lib = load()
     _need(lengths, "lengths", dtype=torch.int32, ndim=1)
     if order is not None:
-        _need(order, "order", device=lengths.device, dtype=torch.int32, ndim=1)
+        _sized(order, "order", lengths.numel(), device=lengths.device, dtype=torch.int32)
     out = torch.empty(3, dtype=torch.int64, device=lengths.device)
-    _check(lib.estp_sjf_padding(_ptr(lengths), _ptr(order), lengths.numel(), int(batch), _ptr(out), _stream(stream)),
-           "estp_sjf_padding")
+    with torch.cuda.device(lengths.device):
+        _check(lib.estp_sjf_padding(_ptr(lengths), _ptr(order), lengths.numel(), int(batch), _ptr(out),
+                                    _stream(stream, lengths.device)),
+               "estp_sjf_padding")
     return out
