@@ -148,19 +148,23 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
     const bool diag = k0 + kKTile - 1 > q0;
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
-      const int qi = q0 + cb * 32 + col;
       if (diag) {
+        // key k0 + rb*32 + 4*half + off(r) lies after query qi iff off(r) > qi - k0 - rb*32 - 4*half,
+        // with off(r) = 8*(r/4) + r%4 a constant: one compare per score, no index arithmetic
+        const int t0 = q0 + cb * 32 + col - k0 - 4 * half;
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (k0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) > qi) acc[rb][cb][r] = -INFINITY;
+            if (8 * (r >> 2) + (r & 3) > t0 - rb * 32) acc[rb][cb][r] = -INFINITY;
       }
-      float sum = s[cb];
+      // four partial sums in a fixed order: no serial chain through one accumulator
+      float s4[4] = {s[cb], 0.f, 0.f, 0.f};
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[rb][cb][r], c2, -m[cb]));
+        for (int r = 0; r < 16; ++r) s4[r & 3] += fast_exp2(fmaf(acc[rb][cb][r], c2, -m[cb]));
+      float sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
       if (!(sum <= 0x1p64f)) {  // overflow, NaN from m = -inf, or far above the reference
         float mx = acc[0][cb][0];
 #pragma unroll
@@ -307,14 +311,15 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
         }
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb) {
-          const int j = k0 + cb * 32 + col;
           float cs = 0.f;
           if (diag) {
+            // query i = i0 + rb*32 + 4*half + off(r) counts for key j iff j < i + 1 - strict, i.e.
+            // off(r) > j - i0 - rb*32 - 4*half - 1 + strict with off(r) = 8*(r/4) + r%4 a constant
+            const int t = k0 + cb * 32 + col - i0 - rb * 32 - 4 * half - 1 + strict;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-              const int i = i0 + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
               const float p = fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
-              cs += (j < i + 1 - strict) ? p : 0.f;
+              cs += (8 * (r >> 2) + (r & 3) > t) ? p : 0.f;
             }
           } else {
 #pragma unroll
