@@ -104,6 +104,52 @@ def recorded_clock(workload: str):
     return (float(g[0]) / 1000.0, float(g[1])) if g else None
 
 
+class HipEvent:
+    """A HIP event recorded on the launch stream for timing only: created with
+    hipEventDisableSystemFence, so recording it does not write back and invalidate the
+    caches (the default event's system-scope fence adds ~6 us of idle time around every
+    call it brackets and cools the cache for the next kernel).  The HIP runtime is the one
+    torch already loaded."""
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self):
+        import ctypes
+        if HipEvent._hip is None:
+            hip = ctypes.CDLL("libamdhip64.so.7")
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._hip = hip
+        self._ev = ctypes.c_void_p()
+        rc = HipEvent._hip.hipEventCreateWithFlags(ctypes.byref(self._ev), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed: {rc}")
+
+    def record(self, stream):
+        rc = HipEvent._hip.hipEventRecord(self._ev, ctypes_stream(stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed: {rc}")
+
+    def elapsed_time(self, other: "HipEvent") -> float:
+        import ctypes
+        ms = ctypes.c_float()
+        rc = HipEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self._ev, other._ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return float(ms.value)
+
+    def __del__(self):
+        if HipEvent._hip is not None and self._ev:
+            HipEvent._hip.hipEventDestroy(self._ev)
+
+
+def ctypes_stream(stream):
+    import ctypes
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
 def row_lse_torch(Q, K, cu_seqlens, scale, torch, rows: int = 1024):
     """Row log-sum-exps [L, Hq, n_tok] of every causal attention row, plain fp32 torch on the
     device, ``rows`` query rows at a time (stands in for what a FlashAttention-style prefill
@@ -209,7 +255,7 @@ def main() -> int:
         torch.cuda.synchronize()
         log(f"warmup step {i + 1}/{args.warmup} done")
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[HipEvent() for _ in range(5)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
@@ -233,7 +279,7 @@ def main() -> int:
                          dtype=torch.uint8, device=X.device)
     S_lse = torch.empty(n_tok, dtype=torch.float32, device=X.device)
     estp.attn_importance_from_lse(Q, K, lse, cu, max_len, S=S_lse, workspace=ws_lse, stream=stream)
-    lse_evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    lse_evs = [HipEvent() for _ in range(6)]
     for k in range(5):
         lse_evs[k].record(stream)
         estp.attn_importance_from_lse(Q, K, lse, cu, max_len, S=S_lse, workspace=ws_lse, stream=stream)
@@ -255,7 +301,7 @@ def main() -> int:
     y_tr = torch.exp(torch.empty(B).uniform_(math.log(16.0), math.log(16384.0), generator=g_tr)).to(X.device)
     pooled_tr = bufs["pooled"]
     estp.head_train_step(pooled_tr, y_tr, edges, centres, theta, m_tr, v_tr, Hd_tr, 1, 0.5, 1e-4, stream=stream)
-    tr_evs = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+    tr_evs = [HipEvent() for _ in range(11)]
     for k in range(10):
         tr_evs[k].record(stream)
         estp.head_train_step(pooled_tr, y_tr, edges, centres, theta, m_tr, v_tr, Hd_tr, k + 2, 0.5, 1e-4,
@@ -273,7 +319,7 @@ def main() -> int:
     yhat_s = estp.predict(bufs["pooled"], *head, workspace=bufs["ws_predict"], stream=stream)
     y_true = torch.exp(torch.empty(B).uniform_(math.log(16.0), math.log(16384.0), generator=g_tr)).to(
         torch.int32).to(X.device)
-    an_evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    an_evs = [HipEvent() for _ in range(3)]
     an_evs[0].record(stream)
     counts = estp.misalignment(H_s, S_s, cu, stream=stream)
     an_evs[1].record(stream)
@@ -292,7 +338,7 @@ def main() -> int:
     # A plain device-to-device copy of X, the bandwidth the pooling call is set against.
     Xc = torch.empty_like(X)
     Xc.copy_(X)
-    cp_evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    cp_evs = [HipEvent() for _ in range(6)]
     for k in range(5):
         cp_evs[k].record(stream)
         Xc.copy_(X)

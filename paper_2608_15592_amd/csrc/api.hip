@@ -2,6 +2,8 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
+
 #include "estp_common.h"
 
 namespace estp {
@@ -16,6 +18,20 @@ void set_error(const char* fmt, ...) {
 }
 
 void clear_error() { g_last_error[0] = '\0'; }
+
+int current_device_cu_count() {
+  static std::atomic<int> cache[kMaxDevices];  // 0 = not yet asked
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev < kMaxDevices) {
+    const int n = cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) return 0;
+  if (dev < kMaxDevices) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
 
 }  // namespace estp
 

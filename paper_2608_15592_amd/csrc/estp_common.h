@@ -114,6 +114,10 @@ __device__ __forceinline__ Ent2 ent2_merge(Ent2 a, Ent2 b) {
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();
 
+// Compute units of the current device (cached per device; 0 when the runtime cannot tell).
+constexpr int kMaxDevices = 64;
+int current_device_cu_count();
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Sequential carving of a caller workspace into 256-byte aligned pieces.

@@ -12,8 +12,11 @@
 // which is exactly sum_i e_i x_i; it also writes the arg-max token and, when
 // asked, the normalised weights e.  With z-scored or min-max scaled inputs a
 // per-prompt statistics pass (zscore_stats_kernel, minmax_stats_kernel) runs
-// first and folds the scaling into u = a1 S + a2 H + c0.  No atomics: results
-// are bitwise reproducible.
+// first and folds the scaling into u = a1 S + a2 H + c0.  Batches of
+// equal-length prompts that fill the chip by themselves take one kernel
+// instead (pool_prompt_kernel: a workgroup streams a whole prompt for one
+// feature slice, so there are no chunk partials to combine).  No atomics:
+// results are bitwise reproducible.
 #include <algorithm>
 
 #include "estp_common.h"
@@ -284,6 +287,103 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
   *reinterpret_cast<float4*>(out + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
 }
 
+// One-kernel pooling of whole prompts: workgroup = (prompt, 512-feature slice),
+// slice fastest.  All 8 waves form the prompt's weights together (u into LDS,
+// workgroup max with its first arg-max, exp-sum Z) while the first rows of X
+// are already in flight; wave w then streams rows w, w + 8, ... of the slice
+// (one 16-byte load per lane and row, 8 rows in flight), reading its weights as
+// LDS broadcasts, and the 8 wave sums are added in wave order and scaled by
+// 1/Z.  No chunk partials, no second kernel.  Used for batches of equal-length
+// prompts that fill the chip by themselves (the host decides).
+constexpr int kPromptThreads = 512;
+constexpr int kPromptWaves = kPromptThreads / 64;
+constexpr int kPromptSlice = 512;     // hidden features per workgroup: 8 per lane
+constexpr int kPromptMaxRows = 8192;  // weights of the prompt staged in LDS (32 KB)
+
+template <typename T>
+__global__ __launch_bounds__(kPromptThreads) void pool_prompt_kernel(
+    const T* __restrict__ X, const float* __restrict__ S, const float* __restrict__ H, const int* __restrict__ cu,
+    int d, int nslices, float a1, float a2, const float4* __restrict__ coef, float* __restrict__ pooled,
+    float* __restrict__ e, int* __restrict__ top) {
+  __shared__ float wts[kPromptMaxRows];
+  __shared__ __attribute__((aligned(16))) float red[kPromptWaves][kPromptSlice];
+  __shared__ float shv[kPromptWaves];
+  __shared__ int shi[kPromptWaves];
+  const int slice = blockIdx.x % nslices;
+  const int b = blockIdx.x / nslices;
+  const int base = cu[b];
+  const int N = min(cu[b + 1] - base, kPromptMaxRows);  // the host guarantees N <= kPromptMaxRows
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = slice * kPromptSlice + lane * 8;
+  const bool active = c < d;
+  const T* xp = X + size_t(base) * d + (active ? c : 0);
+  // rows of this wave: wave, wave + 8, ...
+  const int nw = N > wave ? (N - wave + kPromptWaves - 1) / kPromptWaves : 0;
+
+  constexpr int kInFlight = 8;
+  typename Row8<T>::Raw v[kInFlight];
+  const int n_first = min(nw, kInFlight);
+  if (active) {
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k)
+      if (k < n_first) v[k] = Row8<T>::load(xp + size_t(wave + kPromptWaves * k) * d);
+  }
+
+  // u = a1 S + a2 H + c0 for every token of the prompt, the first arg-max, the exp-sum
+  const float4 cf = coef_of(coef, b, a1, a2);
+  float m = -INFINITY;
+  int mi = 0x7fffffff;
+  for (int i = tid; i < N; i += kPromptThreads) {
+    const float u = fmaf(cf.x, S[base + i], fmaf(cf.y, H[base + i], cf.z));
+    wts[i] = u;
+    if (u > m) {  // increasing i: strict keeps the first
+      m = u;
+      mi = i;
+    }
+  }
+  block_argmax(m, mi, shv, shi);
+  float z = 0.f;
+  for (int i = tid; i < N; i += kPromptThreads) {
+    const float p = fast_exp2((wts[i] - m) * kLog2e);
+    wts[i] = p;
+    z += p;
+  }
+  z = block_sum(z, shv);  // its barriers also publish wts
+  const float invZ = 1.f / z;
+  if (slice == 0) {
+    if (e)
+      for (int i = tid; i < N; i += kPromptThreads) e[base + i] = wts[i] * invZ;
+    if (top && tid == 0) top[b] = base + mi;
+  }
+
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (active) {
+    const float* w = wts + wave;  // weight of the wave's q-th row: w[kPromptWaves * q]
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k)
+      if (k < n_first) Row8<T>::fma8(w[kPromptWaves * k], v[k], acc);
+    int q = n_first;
+    for (; q + kInFlight <= nw; q += kInFlight) {
+#pragma unroll
+      for (int k = 0; k < kInFlight; ++k) v[k] = Row8<T>::load(xp + size_t(wave + kPromptWaves * (q + k)) * d);
+#pragma unroll
+      for (int k = 0; k < kInFlight; ++k) Row8<T>::fma8(w[kPromptWaves * (q + k)], v[k], acc);
+    }
+    for (; q < nw; ++q) Row8<T>::fma8(w[kPromptWaves * q], Row8<T>::load(xp + size_t(wave + kPromptWaves * q) * d), acc);
+  }
+  float* rw = &red[wave][lane * 8];
+  *reinterpret_cast<float4*>(rw) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  *reinterpret_cast<float4*>(rw + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  __syncthreads();
+  const int f = slice * kPromptSlice + tid;
+  if (f < d) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kPromptWaves; ++w) s += red[w][tid];
+    pooled[size_t(b) * d + f] = s * invZ;
+  }
+}
+
 // List of live chunks: entry k = (prompt, chunk) in prompt order, then
 // (-1, 0) up to n_bound.  One workgroup: each thread counts the chunks of a
 // run of consecutive prompts, an exclusive scan over the threads places them.
@@ -423,6 +523,18 @@ size_t live_chunk_bound(int64_t n_tok, int32_t B, int32_t max_seqlen) {
   const size_t nch = (size_t(max_seqlen) + kChunk - 1) / kChunk;
   return std::min(size_t(B) * nch, size_t(n_tok) / kChunk + size_t(B));
 }
+
+// The one-kernel path streams a whole prompt per workgroup, so it needs prompts of
+// (nearly) equal length, short enough for their weights to fit in LDS, and enough
+// (prompt, slice) workgroups to fill every compute unit in equal rounds.
+bool use_prompt_path(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d) {
+  if (max_seqlen > kPromptMaxRows) return false;
+  if (size_t(B) * size_t(max_seqlen) * 8 > size_t(n_tok) * 9) return false;  // > 12.5% below the longest
+  const int n_cu = current_device_cu_count();
+  if (n_cu < 1) return false;
+  const size_t wg = size_t(B) * ((size_t(d) + kPromptSlice - 1) / kPromptSlice);
+  return wg >= size_t(n_cu) && (wg % size_t(n_cu) == 0 || wg >= 4 * size_t(n_cu));
+}
 }  // namespace
 
 extern "C" size_t estp_combine_pool_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d,
@@ -494,6 +606,19 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
     minmax_stats_kernel<<<dim3(B), dim3(1024), 0, s>>>(S, H, cu_seqlens, a1, a2, coef);
     ESTP_CHECK_LAUNCH("minmax_stats_kernel");
     cf = coef;
+  }
+  if (use_prompt_path(n_tok, B, max_seqlen, d)) {
+    const int ns = (d + kPromptSlice - 1) / kPromptSlice;
+    const dim3 pgrid(unsigned(B * ns));
+    if (dtype == ESTP_BF16) {
+      pool_prompt_kernel<uint16_t><<<pgrid, dim3(kPromptThreads), 0, s>>>(
+          static_cast<const uint16_t*>(X), S, H, cu_seqlens, int(d), ns, a1, a2, cf, pooled, e, top);
+    } else {
+      pool_prompt_kernel<float><<<pgrid, dim3(kPromptThreads), 0, s>>>(static_cast<const float*>(X), S, H, cu_seqlens,
+                                                                       int(d), ns, a1, a2, cf, pooled, e, top);
+    }
+    ESTP_CHECK_LAUNCH("pool_prompt_kernel");
+    return ESTP_OK;
   }
   if (use_map) {
     chunk_map_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu_seqlens, B, nch, int(n_bound), map);

@@ -277,6 +277,37 @@ def test_combine_pool_slices_and_reused_workspace():
             check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
 
 
+@pytest.mark.parametrize("xdtype,d,spread,norm", [("bf16", 2040, 10, "none"), ("bf16", 4096, 0, "zscore"),
+                                                 ("f32", 1000, 3, "minmax")])
+def test_combine_pool_equal_prompts_one_kernel(xdtype, d, spread, norm):
+    # prompts of (nearly) equal length whose (prompt, 512-feature slice) workgroups fill
+    # every compute unit four times over: the one-kernel whole-prompt pooling path
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    slices = (d + 511) // 512
+    B = -(-4 * n_cu // slices)
+    g = np.random.default_rng(12 + d)
+    lengths = (100 - g.integers(0, spread + 1, size=B)).tolist()
+    n = sum(lengths)
+    Xf = g.standard_normal((n, d)).astype(np.float32)
+    X = _bf16(Xf) if xdtype == "bf16" else Xf
+    S = (g.random(n) / 30).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    Xd, Sd, Hd, cud = dev(X), dev(S), dev(Hh), dev(cu)
+    for l1, l2, a in [(0.5, 0.5, 1.0), (0.9, 0.1, 0.5)]:
+        pooled, e, top = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
+        e_ref, _ = oracle.combine_weights(S, Hh, cu, l1, l2, a, norm)
+        p_ref = oracle.pool(X, e_ref, cu)
+        np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+        P, top = host(pooled), host(top)
+        for b in range(B):
+            assert rel_l2(P[b], p_ref[b]) <= POOL_RTOL
+            lo, hi = cu[b], cu[b + 1]
+            check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
+        again, _, _ = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
+        assert torch.equal(again, pooled)
+
+
 def test_combine_pool_many_short_prompts():
     # one long prompt and 299 short ones: the pooling runs over the list of live chunks
     # (the full prompt x chunk grid would be mostly empty), built by a scan over prompts
