@@ -5,25 +5,36 @@
 // Layout.  The GEMM is computed transposed, Z^T = W X^T: vocabulary rows are
 // the MFMA "M" side (A operand, rows of W) and tokens the "N" side (B operand,
 // rows of X).  Both operands are contiguous along the hidden dimension d, so
-// every 16-byte global load and every LDS fragment read is a contiguous run
-// of 8 bf16.  In the 32x32 MFMA output a lane owns one token column and 16
-// vocabulary rows, so the per-token reduction over the vocabulary runs in
-// registers with no cross-lane traffic until the very end.
+// every 16-byte transfer and every LDS fragment read is a contiguous run of 8
+// bf16.  The matrix-core step is v_mfma_f32_16x16x32_bf16; in its 16 x 16
+// output a lane owns one token column and 4 consecutive vocabulary rows, so
+// the per-token reduction over the vocabulary runs in registers and needs
+// cross-lane traffic only once, at the very end.
+//
+// Waves.  A workgroup is 4 waves, one per SIMD, on a 256 x 256 tile; wave
+// (wv, wt) owns 128 vocabulary rows x 128 tokens as 8 x 8 blocks of 16 x 16,
+// its 256 fp32 accumulators in AGPRs.  With one wave per SIMD the instruction
+// stream alone decides how busy the matrix core is: every k step issues its
+// 64 MFMAs with the next k step's 16 fragment reads, and after a barrier the
+// 16 transfers into the freed ring slots, spaced one per four MFMAs.  The
+// 16 x 16 step moves a quarter of the accumulator data per MFMA that the 32 x
+// 32 step does, and under this power-limited load the chip holds a higher
+// clock with it.
 //
 // Work split.  A workgroup owns a 256-token tile and a strided subset of the
 // 256-row vocabulary tiles (vocab slice vs takes tiles vs, vs + n_vsplit, ...).
 // Its steps (vocabulary tile, hidden-depth stage) form one flat sequence that
-// an S-deep LDS ring prefetches straight from global memory
-// (global_load_lds_dwordx4, no register staging), across tile boundaries, so
-// the folding of a finished 256 x 256 tile into the running per-token state
-// (max, sum 2^(z2-m), sum 2^(z2-m)(z2-m), base-2 units) overlaps the loads of
-// the next tile.  The n_vsplit partial states per token are merged by a
-// second small kernel that writes H.  Workgroup ids are remapped so the 32
-// workgroups resident on one XCD (ids are dealt round-robin over the 8 XCDs)
-// cover 4 vocabulary slices x 8 token tiles, and one dispatch wave of 256
-// covers 16 x 16: concurrent workgroups stream the same W and X tiles through
-// that XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices
-// that hold one tile more than the others are spread over the XCDs.
+// a ring of LDS part slots prefetches straight from global memory (buffer
+// loads into LDS, no register staging), across tile boundaries, so the
+// folding of a finished tile into the running per-token state (max, sum
+// 2^(z2-m), sum 2^(z2-m)(z2-m), base-2 units) overlaps the loads of the next
+// tile.  The n_vsplit partial states per token are merged by a second small
+// kernel that writes H.  Workgroup ids are remapped so the 32 workgroups
+// resident on one XCD (ids are dealt round-robin over the 8 XCDs) cover 4
+// vocabulary slices x 8 token tiles, and one dispatch wave of 256 covers
+// 16 x 16: concurrent workgroups stream the same W and X tiles through that
+// XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices that
+// hold one tile more than the others are spread over the XCDs.
 #include "estp_common.h"
 
 namespace estp {
@@ -31,84 +42,69 @@ namespace detail {
 
 constexpr int kBV = 256;       // vocabulary rows per tile
 constexpr int kBT = 256;       // tokens per tile
-constexpr int kWaves = 8;      // waves per workgroup, two per SIMD
+constexpr int kWaves = 4;      // waves per workgroup, one per SIMD
 constexpr int kMaxVsplit = 16;
+constexpr int kNB = 8;         // 16-row blocks per wave, both operands (128 rows each)
+constexpr int kMfmaPerStep = kNB * kNB;
 
-// Geometry of one LDS stage (kBV rows of W then kBT rows of X, BK bf16 of the
-// hidden dimension each) and of the wave layout: waves split the 256 x 256
-// tile 2 (vocabulary) x 4 (tokens); a wave owns 128 vocabulary rows x 64 tokens.
-// BK = 64 makes every row of a stage one 128-byte run of global memory, which
-// the texture path fetches as a single request; BK = 32 (64-byte runs) serves
-// hidden sizes that are an odd multiple of 32.
+// Geometry of one LDS stage (kBV rows of W, kBT rows of X, BK bf16 of the
+// hidden dimension each).  BK = 64 makes every row of a stage one 128-byte run
+// of global memory, which the texture path fetches as a single request; BK =
+// 32 (64-byte runs) serves hidden sizes that are an odd multiple of 32.
 template <int BK>
 struct Geom {
-  static constexpr int kThreads = kWaves * 64;
-  static constexpr int TW = 2 * kBT / kWaves;                       // 64 tokens per wave
-  static constexpr int JT = TW / 32;                                // 32-token MFMA blocks per wave
-  static constexpr int kSub = BK / 16;                              // 16-deep MFMA steps per stage
+  static constexpr int kSub = BK / 32;                              // 32-deep MFMA steps per stage
   static constexpr int kRowBytes = BK * 2;                          // 64 or 128 B
   static constexpr int kChunks = kRowBytes / 16;                    // 16-byte chunks per row
-  static constexpr int kRowsPerInst = 64 / kChunks;                 // rows per wave instruction (1 KB)
-  static constexpr int kInstW = kBV / (kRowsPerInst * kWaves);      // W transfers per wave per stage
-  static constexpr int kInstX = kBT / (kRowsPerInst * kWaves);      // X transfers per wave per stage
-  static constexpr int kLoadsPerStage = kInstW + kInstX;            // vector-memory instructions per wave
+  static constexpr int kRowsPerInst = 64 / kChunks;                 // rows per wave transfer (1 KB)
+  static constexpr int L = kBV / (kRowsPerInst * kWaves);           // transfers per wave per part
   static constexpr int kPartBytes = kBV * kRowBytes;                // one operand of one stage (kBV == kBT)
   static constexpr int kRowsPerWindow = 256 / kRowBytes;            // rows that share a 256-byte bank window
   // Chunk swizzle: the 16 rows that 16 consecutive lanes read at one logical
-  // chunk land in 16 distinct 16-byte bank groups.
+  // chunk land in 16 distinct 16-byte bank groups.  It depends on the row only
+  // through (row / kRowsPerWindow) % kChunks, which repeats every 16 rows.
   __device__ static __forceinline__ int swz(int row, int chunk) {
     return chunk ^ ((row / kRowsPerWindow) & (kChunks - 1));
   }
 };
 
-// One 16-deep k step of a wave's tile: 4 A fragments (vocabulary rows) and
-// JT B fragments (tokens), 8 bf16 each.
-template <int JT>
-struct Frags {
-  bf16x8_t a[4], b[JT];
-};
+// Spacing of the instructions threaded between the 64 MFMAs of a k step:
+// fragment read q after MFMA kReadEvery * q, transfer t after MFMA
+// kDmaFirst + kDmaEvery * t.  Evenly spread, neither kind ever holds the wave
+// away from the matrix core for long (measured: reading all 16 fragments over
+// the first 16 MFMAs ran ~6% slower).
+constexpr int kReadEvery = 4, kDmaFirst = 2, kDmaEvery = 4;
 
-// Scheduling hint for one k step: its LDS fragment reads go out two per MFMA
-// at the front, so each has at least the remaining MFMAs of the step to land.
-template <int kReads, int kMfma>
-__device__ __forceinline__ void schedule_reads_front() {
-  constexpr int kGroups = (kReads + 1) / 2;
-#pragma unroll
-  for (int q = 0; q < kGroups; ++q) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kGroups, 0);
+__device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// Ring of P part slots.  A stage (BK deep) has two parts, its W rows and its
-// X rows; part 2s + 0 / 2s + 1 (W / X of stage s) lives in slot (2s + o) % P.
-// Within a stage the wave runs kSub k steps, each reading the next step's
-// fragments while its MFMAs run.  Before the last k step every wave waits for
-// its own fragment reads (so stage s is no longer read) and for stage s + 1 to
-// have landed, then one barrier; after it the two freed slots take parts
-// 2s + P and 2s + P + 1.  With P odd the W part of a stage is issued one stage
-// before its X part, and about (P - 2) / 2 stages of loads are in flight
-// while a stage is consumed.
-template <int P, int BK, bool SPLIT>
-__global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
+// A stage is BK deep (kSub k steps).  Ring of P part slots: part 2s + 0 / 2s + 1
+// (W / X of stage s) lives in slot (2s + o) % P.  Within a stage the wave runs
+// kSub k steps, each reading the next step's fragments while its MFMAs run.
+// Before the last k step every wave waits for its own fragment reads (so stage
+// s is no longer read) and for stage s + 1 to have landed, then one barrier;
+// after it the two freed slots take parts 2s + P and 2s + P + 1.  With P odd
+// the W part of a stage is issued one stage before its X part, and about
+// (P - 2) / 2 stages of loads are in flight while a stage is consumed.
+template <int P, int BK>
+__global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
     int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
   using G = Geom<BK>;
-  constexpr int JT = G::JT;
-  static_assert(kBV == kBT, "W and X parts share one slot size");
-  static_assert(P >= 4, "the ring needs at least two stages");
-  static_assert(G::kSub >= 2, "the barrier sits between the last two k steps of a stage");
-  static_assert(G::kInstW == G::kInstX, "equal load counts per part");
-  static_assert(4 * G::JT >= 2 * G::kInstW, "one transfer per MFMA of a k step");
-  constexpr int L = G::kInstW;  // vector-memory instructions per wave per part
+  constexpr int L = G::L;
+  constexpr int kSub = G::kSub;
+  constexpr int kBlockBytes = 16 * G::kRowBytes;
+  static_assert(P >= 4 && P % 2 == 1, "the ring needs two stages and an odd slot count");
+  static_assert(kReadEvery * (2 * kNB - 1) < kMfmaPerStep, "fragment reads fit in a k step");
+  static_assert(kDmaFirst + kDmaEvery * (2 * L - 1) < kMfmaPerStep, "transfers fit in a k step");
   __shared__ __attribute__((aligned(16))) char lds[P * G::kPartBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave & 1;   // which 128-row half of the vocabulary tile
-  const int wt = wave >> 1;  // which TW-token slice of the token tile
+  const int wt = wave >> 1;  // which 128-token half of the token tile
 
   // ---- workgroup -> (vocabulary slice, token tile)
   int vs, tt;
@@ -129,193 +125,182 @@ __global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
   const int n_my_tiles = (n_vt - vs + n_vsplit - 1) / n_vsplit;
   const size_t row_stride = size_t(d) * 2;  // bytes per row of W and X
 
-  // ---- staging: lane l of instruction i fills row kRowsPerInst*(kWaves i + wave) + l / kChunks,
-  // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.
-  int st_row[G::kInstW];
-  uint32_t st_chunk_off[G::kInstW], offx[G::kInstX];
-  const char* xt = reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride;
+  // ---- staging: lane l of transfer i fills row kRowsPerInst*(kWaves i + wave) + l / kChunks,
+  // physical chunk l % kChunks, i.e. logical chunk swz(row, l % kChunks) of that row.  The
+  // transfers go through buffer resources that cover exactly the live rows of a tile (W: the
+  // vocabulary tile, X: the token tile), so rows past V or n_tok read as zero with no clamping;
+  // each transfer is one instruction: per-lane byte offset in the tile (fixed for the whole
+  // kernel) + the stage's depth offset in a scalar register.
+  uint32_t st_off[L];
 #pragma unroll
-  for (int i = 0; i < G::kInstW; ++i) {
-    st_row[i] = G::kRowsPerInst * (kWaves * i + wave) + lane / G::kChunks;
-    st_chunk_off[i] = uint32_t(G::swz(st_row[i], lane % G::kChunks) * 16);
+  for (int i = 0; i < L; ++i) {
+    const int row = G::kRowsPerInst * (kWaves * i + wave) + lane / G::kChunks;
+    st_off[i] = uint32_t(row) * uint32_t(row_stride) + uint32_t(G::swz(row, lane % G::kChunks) * 16);
   }
-#pragma unroll
-  for (int i = 0; i < G::kInstX; ++i) {
-    const int tr = min(tt * kBT + st_row[i], n_tok - 1) - tt * kBT;
-    offx[i] = uint32_t(tr) * uint32_t(row_stride) + st_chunk_off[i];
-  }
+  const uint32_t tile_bytes = uint32_t(kBV) * uint32_t(row_stride);
+  const buf_rsrc_t rx = make_rsrc(reinterpret_cast<const char*>(X) + size_t(tt) * kBT * row_stride,
+                                  uint32_t(min(kBT, n_tok - tt * kBT)) * uint32_t(row_stride));
 
   // ---- prefetch of parts in order 0, 1, 2, ...: part q is operand q % 2 of
-  // stage q / 2 = (tile, ks).  Parts past the end re-load the last stage into
-  // the slot being freed (never read), so every barrier issues exactly 2 L
-  // loads per wave and the waits below are the same on every stage; the loop
-  // body stays one basic block.
+  // stage q / 2 = (tile, ks).  Parts past the end are issued with an empty
+  // resource (no memory access, zeros into the slot being freed, never read),
+  // so every barrier issues exactly 2 L transfers per wave and the waits below
+  // are the same on every stage; the loop body stays one basic block.
   int pf_tile = 0, pf_ks = 0, pf_slot = 0, pf_op = 0;
-  // Source and destination of the next part; advances the part counters.
+  int pf_vt = vs;                                                                  // vocabulary tile of the prefetch
+  const char* pf_w = reinterpret_cast<const char*>(W) + size_t(vs) * tile_bytes;  // its rows of W
+  const size_t w_step = size_t(n_vsplit) * tile_bytes;
+  const buf_rsrc_t r_none = make_rsrc(X, 0u);
   struct Part {
-    const char* src;  // W: start of the vocabulary tile's rows at depth ks; X: same for the token tile
+    buf_rsrc_t rsrc;  // the vocabulary tile's rows of W, or the token tile's rows of X
+    uint32_t soff;    // depth offset of the stage inside a row
     char* dst;        // this wave's first 1 KB block of the slot
-    int vt;           // vocabulary tile (W parts)
   };
+  // Source and destination of the next part; advances the part counters.
   auto next_part = [&](int op) {
     const bool live = pf_tile < n_my_tiles;
-    const int ks = live ? pf_ks : nk - 1;
     Part p;
     p.dst = lds + pf_slot * G::kPartBytes + G::kRowsPerInst * wave * G::kRowBytes;
-    p.vt = vs + (live ? pf_tile : n_my_tiles - 1) * n_vsplit;
+    p.soff = uint32_t(pf_ks) * G::kRowBytes;
     if (op == 0) {
-      p.src = reinterpret_cast<const char*>(W) + size_t(p.vt) * kBV * row_stride + size_t(ks) * G::kRowBytes;
+      // past the last tile pf_w points beyond W, but the empty resource never reads it
+      const uint32_t rows = live ? uint32_t(min(kBV, V - pf_vt * kBV)) : 0u;
+      p.rsrc = make_rsrc(pf_w, rows * uint32_t(row_stride));
     } else {
-      p.src = xt + size_t(ks) * G::kRowBytes;
+      p.rsrc = live ? rx : r_none;
       const bool wrap = pf_ks + 1 == nk;
       pf_ks = wrap ? 0 : pf_ks + 1;
-      pf_tile = wrap ? pf_tile + 1 : pf_tile;
+      if (wrap) {
+        ++pf_tile;
+        pf_vt += n_vsplit;
+        pf_w += w_step;
+      }
     }
     pf_slot = pf_slot + 1 == P ? 0 : pf_slot + 1;
     return p;
   };
   // Transfer i (of L) of a part: 1 KB, kRowsPerInst rows.
-  auto dma_one = [&](const Part& p, int op, int i) {
-    char* dst = p.dst + G::kRowsPerInst * kWaves * i * G::kRowBytes;
-    if (op == 0) {
-      const int vr = min(p.vt * kBV + st_row[i], V - 1) - p.vt * kBV;
-      lds_dma16(p.src + (uint32_t(vr) * uint32_t(row_stride) + st_chunk_off[i]), dst);
-    } else {
-      lds_dma16(p.src + offx[i], dst);
-    }
+  auto dma_one = [&](const Part& p, int i) {
+    lds_dma16_buf(p.rsrc, st_off[i], p.soff, p.dst + G::kRowsPerInst * kWaves * i * G::kRowBytes);
   };
   auto issue_part = [&]() {
-    const int op = pf_op;
-    const Part p = next_part(op);
+    const Part p = next_part(pf_op);
 #pragma unroll
-    for (int i = 0; i < L; ++i) dma_one(p, op, i);
+    for (int i = 0; i < L; ++i) dma_one(p, i);
     pf_op ^= 1;
   };
   // The two parts issued at every barrier: their operands are fixed, since an
   // even number of parts precedes each barrier's pair.
   constexpr int kOpA = P % 2, kOpB = kOpA ^ 1;
 
-  // ---- fragment reads: lane (row r = lane % 32, half h = lane / 32) reads 8 bf16 at
-  // k offset 16 kk + 8 h of row r of each 32-row block.
-  const int frag_row = lane & 31;
-  const int frag_half = lane >> 5;
-  uint32_t fa_off[G::kSub][4], fb_off[G::kSub][JT];  // byte offsets inside a stage, per k step
+  // ---- fragment reads: lane (r = lane % 16, q = lane / 16) reads 8 bf16 at k offset
+  // 32 kk + 8 q of row r of each 16-row block.  The swizzle is the same in every
+  // 16-row block, so one offset per k step serves all 8 blocks, 16 rows apart.
+  const int fr = lane & 15, fq = lane >> 4;
+  uint32_t fa_off[kSub], fb_off[kSub];
 #pragma unroll
-  for (int kk = 0; kk < G::kSub; ++kk) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ra = wv * 128 + i * 32 + frag_row;
-      fa_off[kk][i] = ra * G::kRowBytes + G::swz(ra, kk * 2 + frag_half) * 16;
-    }
-#pragma unroll
-    for (int j = 0; j < JT; ++j) {
-      const int rb = wt * G::TW + j * 32 + frag_row;
-      fb_off[kk][j] = rb * G::kRowBytes + G::swz(rb, kk * 2 + frag_half) * 16;
-    }
+  for (int kk = 0; kk < kSub; ++kk) {
+    const int ra = wv * 128 + fr, rb = wt * 128 + fr;
+    fa_off[kk] = ra * G::kRowBytes + G::swz(ra, kk * 4 + fq) * 16;
+    fb_off[kk] = rb * G::kRowBytes + G::swz(rb, kk * 4 + fq) * 16;
   }
-  auto read_frags = [&](Frags<JT>& f, int slot_w, int slot_x, int kk) {
-    const char* bw = lds + slot_w * G::kPartBytes;
-    const char* bx = lds + slot_x * G::kPartBytes;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(bw + fa_off[kk][i]);
-#pragma unroll
-    for (int j = 0; j < JT; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(bx + fb_off[kk][j]);
+  struct Frags {
+    bf16x8_t a[kNB], b[kNB];  // vocabulary-row blocks, token blocks
   };
-  constexpr int kReads = 4 + JT;       // LDS reads per k step
-  constexpr int kMfma = 4 * JT;        // MFMAs per k step
+  // fragment q of 2 kNB: the A blocks first, then the B blocks
+  auto read_frag = [&](Frags& f, int slot_w, int slot_x, int kk, int q) {
+    if (q < kNB)
+      f.a[q] = *reinterpret_cast<const bf16x8_t*>(lds + slot_w * G::kPartBytes + fa_off[kk] + q * kBlockBytes);
+    else
+      f.b[q - kNB] = *reinterpret_cast<const bf16x8_t*>(lds + slot_x * G::kPartBytes + fb_off[kk] +
+                                                        (q - kNB) * kBlockBytes);
+  };
 
-  // ---- per-lane entropy state for the JT token columns this lane owns
-  Ent2 st[JT];
+  // ---- per-lane entropy state for the kNB token columns this lane owns
+  Ent2 st[kNB];
 #pragma unroll
-  for (int cb = 0; cb < JT; ++cb) st[cb] = Ent2{-INFINITY, 0.f, 0.f};
+  for (int j = 0; j < kNB; ++j) st[j] = Ent2{-INFINITY, 0.f, 0.f};
 
   // ---- prologue: the first parts in flight; wait for stage 0, read its first fragments
-  constexpr int kPrologue = SPLIT ? P - 1 : P;
 #pragma unroll
-  for (int q = 0; q < kPrologue; ++q) issue_part();
-  wait_vm<(kPrologue - 2) * L>();
+  for (int q = 0; q < P; ++q) issue_part();
+  wait_vm<(P - 2) * L>();
   lds_barrier();
-  Frags<JT> f[2];
-  read_frags(f[0], 0, 1, 0);
+  // With two k steps per stage the buffers alternate inside the stage and stage
+  // s + 1 starts in f[0]; with one, each stage starts by moving the fragments
+  // read during the previous stage from f[1] into f[0].
+  Frags f[2];
+  constexpr int kFirst = kSub == 1 ? 1 : 0;
+#pragma unroll
+  for (int q = 0; q < 2 * kNB; ++q) read_frag(f[kFirst], 0, 1, 0, q);
   int sw = 0;  // slot of the W part of the current stage; its X part is in sw + 1 (mod P)
 
-  // MFMAs of one k step with the L transfers of part p0 and then, if n1 > 0,
-  // those of part p1 threaded between them, one per MFMA, so a burst of
-  // transfers never holds the wave away from the matrix core.
-  auto mfma_with_dma = [&](f32x16_t(&acc)[4][JT], const Frags<JT>& cur, const Part& p0, int op0, const Part& p1,
-                           int op1, int n1) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < JT; ++j) {
-        const int m = i * JT + j;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[i], cur.b[j], acc[i][j], 0, 0, 0);
-        if (m < L)
-          dma_one(p0, op0, m);
-        else if (m < L + n1)
-          dma_one(p1, op1, m - L);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-  };
-
   for (int tile = 0; tile < n_my_tiles; ++tile) {
-    f32x16_t acc[4][JT];
+    f32x4_t acc[kNB][kNB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kNB; ++i)
 #pragma unroll
-      for (int j = 0; j < JT; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int j = 0; j < kNB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     for (int ks = 0; ks < nk; ++ks) {
       const int sx = sw + 1 == P ? 0 : sw + 1;
       const int sw_next = sx + 1 == P ? 0 : sx + 1;
       const int sx_next = sw_next + 1 == P ? 0 : sw_next + 1;
+      Part pa, pb;  // the two parts issued after this stage's barrier
 #pragma unroll
-      for (int u = 0; u < G::kSub; ++u) {
-        Frags<JT>& cur = f[u & 1];
-        Frags<JT>& nxt = f[(u + 1) & 1];
-        if (u + 1 < G::kSub) {
-          read_frags(nxt, sw, sx, u + 1);
-          if (SPLIT && u == 0) {
-            // the second part freed at the previous barrier goes out here
-            const Part pb = next_part(kOpB);
-            mfma_with_dma(acc, cur, pb, kOpB, pb, kOpB, 0);
-            continue;
-          }
-        } else {
+      for (int u = 0; u < kSub; ++u) {
+        Frags& cur = f[u & 1];
+        Frags& nxt = f[(u + 1) & 1];
+        const bool last = u + 1 == kSub;
+        if (last) {
           // This wave's reads of the stage are done (lgkmcnt 0 inside the
           // barrier) and the next stage has landed (only the P - 4 parts
           // issued after it may still be in flight): after the barrier nobody
           // reads this stage's slots again, so they take the next two parts.
-          // The previous k step's MFMAs stay in front of the wait.
+          if (kSub == 1) {
+            pa = next_part(kOpA);
+            pb = next_part(kOpB);
+          }
           __builtin_amdgcn_sched_barrier(0);
           wait_vm<(P - 4) * L>();
           lds_barrier();
-          const Part pa = next_part(kOpA);
-          if (SPLIT) {
-            read_frags(nxt, sw_next, sx_next, 0);  // past the last stage: read and never used
-            mfma_with_dma(acc, cur, pa, kOpA, pa, kOpA, 0);
-          } else {
-            const Part pb = next_part(kOpB);
-            read_frags(nxt, sw_next, sx_next, 0);  // past the last stage: read and never used
-            mfma_with_dma(acc, cur, pa, kOpA, pb, kOpB, L);
-          }
-          continue;
+          if (kSub == 1) f[0] = f[1];
+        } else if (u + 2 == kSub) {
+          // scalar set-up of the parts issued after the coming barrier
+          pa = next_part(kOpA);
+          pb = next_part(kOpB);
         }
+        // the MFMAs of this k step, with the next k step's fragment reads (past
+        // the last stage: read and never used) and, after the barrier, the
+        // transfers into the freed slots threaded between them
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kNB; ++i)
 #pragma unroll
-          for (int j = 0; j < JT; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[i], cur.b[j], acc[i][j], 0, 0, 0);
-        schedule_reads_front<kReads, kMfma>();
+          for (int j = 0; j < kNB; ++j) {
+            const int m = i * kNB + j;
+            acc[i][j] = mfma16(cur.a[i], cur.b[j], acc[i][j]);
+            if (m % kReadEvery == 0 && m / kReadEvery < 2 * kNB) {
+              if (last)
+                read_frag(nxt, sw_next, sx_next, 0, m / kReadEvery);
+              else
+                read_frag(nxt, sw, sx, u + 1, m / kReadEvery);
+            }
+            if (last && m >= kDmaFirst && (m - kDmaFirst) % kDmaEvery == 0 && (m - kDmaFirst) / kDmaEvery < 2 * L) {
+              const int t = (m - kDmaFirst) / kDmaEvery;
+              if (t < L)
+                dma_one(pa, t);
+              else
+                dma_one(pb, t - L);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
       }
       sw = sw_next;
     }
 
     // ---- fold the finished tile into the running states.  acc[i][j][r] is the
-    // logit of vocabulary row vt*256 + wv*128 + i*32 + 8*(r/4) + 4*frag_half + r%4
-    // for token tt*BT + wt*TW + j*32 + frag_row.
+    // logit of vocabulary row vt*256 + wv*128 + 16 i + 4 fq + r for token
+    // tt*256 + wt*128 + 16 j + fr.
     //
     // The state (m, s, t) is kept relative to a reference m that is the running
     // log-sum-exp after each tile (rebased so that s = 1).  Full tiles are then
@@ -325,32 +310,30 @@ __global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
     // takes the exact, masked path.
     const int vt = vs + tile * n_vsplit;
     const bool ragged = (vt + 1) * kBV > V;
-    const int lim = V - (vt * kBV + wv * 128 + 4 * frag_half);  // live rows: offset < lim
+    const int lim = V - (vt * kBV + wv * 128 + 4 * fq);  // live rows: 16 i + r < lim
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
+    for (int j = 0; j < kNB; ++j) {
       Ent2 e = st[j];
       bool exact = ragged;
       if (!ragged) {
         if (tile == 0) {  // first tile: the tile's own max is the reference
           float mx = acc[0][j][0];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < kNB; ++i)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[i][j][r]);
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[i][j][r]);
           e = Ent2{mx * kLog2e, 0.f, 0.f};
         }
         float s = e.s, t = e.t;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < kNB; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
+          for (int r = 0; r < 4; ++r) {
             const float dd = fmaf(acc[i][j][r], kLog2e, -e.m);
             const float p = fast_exp2(dd);
             s += p;
             t = fmaf(p, dd, t);
           }
-          __builtin_amdgcn_sched_barrier(0);  // block by block: bounds live copies
-        }
         if (s <= 0x1p64f) {
           e.s = s;
           e.t = t;
@@ -361,24 +344,24 @@ __global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
       if (exact) {
         float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kNB; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const bool live = !ragged || i * 32 + 8 * (r >> 2) + (r & 3) < lim;
+          for (int r = 0; r < 4; ++r) {
+            const bool live = !ragged || i * 16 + r < lim;
             mx = live ? fmaxf(mx, acc[i][j][r]) : mx;
           }
         const float mnew = fmaxf(e.m, mx * kLog2e);
         const float dl = fmaxf(e.m - mnew, kExp2Floor);
-        const float f = fast_exp2(dl);
-        float s = f * e.s;
-        float t = f * (e.t + e.s * dl);
+        const float sc = fast_exp2(dl);
+        float s = sc * e.s;
+        float t = sc * (e.t + e.s * dl);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kNB; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
+          for (int r = 0; r < 4; ++r) {
             // dead rows enter as -inf: dd clamps to the floor and adds 0 * floor,
             // also while mnew is still -inf (a lane with no live row yet)
-            const bool live = !ragged || i * 32 + 8 * (r >> 2) + (r & 3) < lim;
+            const bool live = !ragged || i * 16 + r < lim;
             const float dd = fmaxf(fmaf(live ? acc[i][j][r] : -INFINITY, kLog2e, -mnew), kExp2Floor);
             const float p = fast_exp2(dd);
             s += p;
@@ -396,32 +379,35 @@ __global__ __launch_bounds__(kWaves * 64, 2) void entropy_gemm_kernel(
     }
   }  // tile
 
-  // ---- lanes l and l+32 hold the same tokens: merge them
+  // ---- lanes l, l ^ 16, l ^ 32 and l ^ 48 hold the same tokens: merge them
 #pragma unroll
-  for (int j = 0; j < JT; ++j) {
-    Ent2 o;
-    o.m = __shfl_xor(st[j].m, 32, 64);
-    o.s = __shfl_xor(st[j].s, 32, 64);
-    o.t = __shfl_xor(st[j].t, 32, 64);
-    st[j] = ent2_merge(st[j], o);
+  for (int j = 0; j < kNB; ++j) {
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      Ent2 x;
+      x.m = __shfl_xor(st[j].m, o, 64);
+      x.s = __shfl_xor(st[j].s, o, 64);
+      x.t = __shfl_xor(st[j].t, o, 64);
+      st[j] = ent2_merge(st[j], x);
+    }
   }
   // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS
   __syncthreads();  // every wave is done with the ring (no loads remain in flight)
   float* xbuf = reinterpret_cast<float*>(lds);  // [BT tokens][3]
-  if (wv == 1 && frag_half == 0) {
+  if (wv == 1 && fq == 0) {
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
-      float* p = xbuf + (wt * G::TW + j * 32 + frag_row) * 3;
+    for (int j = 0; j < kNB; ++j) {
+      float* p = xbuf + (wt * 128 + j * 16 + fr) * 3;
       p[0] = st[j].m;
       p[1] = st[j].s;
       p[2] = st[j].t;
     }
   }
   __syncthreads();
-  if (wv == 0 && frag_half == 0) {
+  if (wv == 0 && fq == 0) {
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
-      const int tl = wt * G::TW + j * 32 + frag_row;
+    for (int j = 0; j < kNB; ++j) {
+      const int tl = wt * 128 + j * 16 + fr;
       const float* p = xbuf + tl * 3;
       Ent2 r = ent2_merge(st[j], Ent2{p[0], p[1], p[2]});
       const int tok = tt * kBT + tl;
@@ -507,9 +493,9 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   const uint16_t* Xh = static_cast<const uint16_t*>(X);
   const uint16_t* Wh = static_cast<const uint16_t*>(W);
   if (d % 64 == 0)
-    entropy_gemm_kernel<5, 64, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+    entropy_gemm_kernel<5, 64><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
   else
-    entropy_gemm_kernel<7, 32, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
+    entropy_gemm_kernel<9, 32><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
   ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");

@@ -30,6 +30,24 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* dst_wave_base) 
 #endif
 }
 
+// Buffer resource (V#) over `bytes` bytes from `base`: raw dword addressing
+// (stride 0); a lane whose byte offset is at or past `bytes` reads zero and
+// touches no memory.  Word 3 is the gfx9 data-format word for dword access.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc_t;
+__device__ __forceinline__ buf_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, int(bytes), 0x00020000);
+}
+
+// 16-byte buffer -> LDS transfer (buffer_load_dwordx4 ... lds): lane l reads
+// the 16 bytes at voffset(l) + soffset of the resource; they land in LDS at
+// dst_wave_base + 16 * l.  `soffset` and `dst_wave_base` must be uniform.
+__device__ __forceinline__ void lds_dma16_buf(buf_rsrc_t r, uint32_t voffset, uint32_t soffset,
+                                              void* dst_wave_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, to_lds(dst_wave_base), 16, voffset, soffset, 0, 0);
+#endif
+}
+
 // s_waitcnt vmcnt(N): wait until at most N of this wave's vector-memory
 // operations are outstanding (they retire in issue order), including global ->
 // LDS transfers; other counters untouched.  gfx9 encoding: vmcnt[3:0] |
