@@ -99,7 +99,8 @@ ESTP_API const char* estp_last_error(void);
  *   dtype          ESTP_BF16 (ESTP_F32 returns ESTP_ERR_UNSUPPORTED)
  * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0; a d that is not a
  * multiple of 32 returns ESTP_ERR_UNSUPPORTED (the matrix-core k steps are
- * 16 deep and a stage row is at least 64 bytes).
+ * 32 deep), as does 512 d >= 2^32 (a 256-row tile of W must be addressable
+ * with 32-bit offsets).
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype);
 ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
