@@ -74,6 +74,7 @@ struct Geom {
 // away from the matrix core for long (measured: reading all 16 fragments over
 // the first 16 MFMAs ran ~6% slower).
 constexpr int kReadEvery = 4, kDmaFirst = 2, kDmaEvery = 4;
+constexpr int kSetupA = 5, kSetupB = 37;  // MFMAs after which the next parts' scalar set-up runs
 
 __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -265,10 +266,6 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
           wait_vm<(P - 4) * L>();
           lds_barrier();
           if (kSub == 1) f[0] = f[1];
-        } else if (u + 2 == kSub) {
-          // scalar set-up of the parts issued after the coming barrier
-          pa = next_part(kOpA);
-          pb = next_part(kOpB);
         }
         // the MFMAs of this k step, with the next k step's fragment reads (past
         // the last stage: read and never used) and, after the barrier, the
@@ -279,6 +276,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
           for (int j = 0; j < kNB; ++j) {
             const int m = i * kNB + j;
             acc[i][j] = mfma16(cur.a[i], cur.b[j], acc[i][j]);
+            // scalar set-up of the parts issued after the coming barrier, each behind
+            // an MFMA of the k step before it
+            if (u + 2 == kSub && m == kSetupA) pa = next_part(kOpA);
+            if (u + 2 == kSub && m == kSetupB) pb = next_part(kOpB);
             if (m % kReadEvery == 0 && m / kReadEvery < 2 * kNB) {
               if (last)
                 read_frag(nxt, sw_next, sx_next, 0, m / kReadEvery);
