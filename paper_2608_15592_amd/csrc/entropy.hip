@@ -392,8 +392,11 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
       st[j] = ent2_merge(st[j], x);
     }
   }
-  // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS
-  __syncthreads();  // every wave is done with the ring (no loads remain in flight)
+  // ---- the two vocabulary halves (wv = 0, 1) hold the same tokens: merge through LDS.
+  // The transfers issued at the last barrier (empty parts past the end, which still write
+  // zeros into their slots) must land before slot 0 is reused.
+  wait_vm<0>();
+  __syncthreads();  // every wave is done with the ring and no transfer remains in flight
   float* xbuf = reinterpret_cast<float*>(lds);  // [BT tokens][3]
   if (wv == 1 && fq == 0) {
 #pragma unroll
