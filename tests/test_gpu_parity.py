@@ -306,6 +306,9 @@ def test_combine_pool_equal_prompts_one_kernel(xdtype, d, spread, norm):
             check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
         again, _, _ = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
         assert torch.equal(again, pooled)
+        # without the optional weights and top-token outputs
+        bare, e0, t0 = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm, want_e=False, want_top=False)
+        assert e0 is None and t0 is None and torch.equal(bare, pooled)
 
 
 def test_combine_pool_many_short_prompts():
