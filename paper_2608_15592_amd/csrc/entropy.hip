@@ -112,14 +112,18 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
   {
     const int bid = blockIdx.x;
     constexpr int R = 32;  // workgroups resident on one XCD
-    if (n_vsplit == 16 && (n_tt % (R / 2)) == 0) {
+    // whole dispatch waves of 16 token tiles x 16 slices take the XCD-aware order; the
+    // token tiles past the last whole group of 16 (ragged batches) follow in plain order
+    const int n_full = n_vsplit == 16 ? (n_tt / (R / 2)) * (R / 2) * 16 : 0;
+    if (bid < n_full) {
       const int xcd = bid & 7, j = bid >> 3;
       const int wave_idx = j / R, jj = j % R;
       vs = (jj & 3) * 4 + (xcd & 3);
       tt = wave_idx * (R / 2) + (xcd >> 2) * (R / 4) + (jj >> 2);
     } else {
-      vs = bid % n_vsplit;
-      tt = bid / n_vsplit;
+      const int r = bid - n_full;
+      vs = r % n_vsplit;
+      tt = n_full / n_vsplit + r / n_vsplit;
     }
   }
   const int nk = d / BK;
