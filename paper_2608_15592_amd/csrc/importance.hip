@@ -36,6 +36,13 @@ constexpr int kKTile = 64;     // keys per streamed tile in pass 1
 constexpr int kQTile = 64;     // queries per streamed tile in pass 2 (two 32-query row blocks in turn)
 static_assert(kKBlock % kQTile == 0 && kQTile % 32 == 0, "pass-2 tiles must tile a key block");
 
+// Upper bound on the live 256-row blocks: sum_b ceil(N_b / 256) <= n_tok / 256 + B.
+inline size_t block_bound(int64_t n_tok, int32_t B, int32_t max_seqlen) {
+  const size_t nblk = (size_t(max_seqlen) + kQBlock - 1) / kQBlock;
+  const size_t a = size_t(B) * nblk, c = size_t(n_tok) / kQBlock + size_t(B);
+  return a < c ? a : c;
+}
+
 // Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
 // consecutive rows read at one logical chunk hit 16 distinct bank groups.
 template <int DH>
@@ -69,6 +76,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
                                                             const uint16_t* __restrict__ K,
                                                             const int* __restrict__ cu, int B, int n_tok,
                                                             int L, int Hq, int Hkv, int nqb_max, float c2,
+                                                            const int2* __restrict__ blist,
                                                             float* __restrict__ lse2) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
@@ -76,11 +84,21 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
   __shared__ __attribute__((aligned(16))) char ktile[2][kTileBytes];
 
   // block -> (query block, prompt, layer * Hq + head); largest query blocks first
+  // or, when many prompts are much shorter than the longest, the entry of the list of live
+  // 256-row blocks (already heaviest first)
   int idx = blockIdx.x;
   const int lh = idx % (L * Hq);
   idx /= L * Hq;
-  const int b = idx % B;
-  const int qblk = nqb_max - 1 - idx / B;
+  int b, qblk;
+  if (blist) {
+    const int2 e = blist[idx];
+    if (e.x < 0) return;  // past the live blocks
+    b = e.x;
+    qblk = e.y;
+  } else {
+    b = idx % B;
+    qblk = nqb_max - 1 - idx / B;
+  }
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   if (qblk * kQBlock >= N) return;
@@ -208,7 +226,8 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
                                                                const int* __restrict__ cu, int B, int n_tok,
                                                                int L, int Hq, int Hkv, float c2,
                                                                const float* __restrict__ lse2, float lse_mul,
-                                                               int strict, float* __restrict__ part) {
+                                                               int strict, const int2* __restrict__ blist,
+                                                               int n_blist, float* __restrict__ part) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
   constexpr int kTileBytes = kQTile * T::kRowBytes;
@@ -217,11 +236,21 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
 
   const int G = Hq / Hkv;
   // block -> (key block, prompt, layer * Hkv + kv head); key block 0 (the most work) first
+  // or the list of live 256-row blocks walked from its end (lightest first there, so heaviest
+  // first here; the padding entries past the live ones come first and exit at once)
   int idx = blockIdx.x;
   const int lg = idx % (L * Hkv);
   idx /= L * Hkv;
-  const int b = idx % B;
-  const int kblk = idx / B;
+  int b, kblk;
+  if (blist) {
+    const int2 e = blist[n_blist - 1 - idx];
+    if (e.x < 0) return;
+    b = e.x;
+    kblk = e.y;
+  } else {
+    b = idx % B;
+    kblk = idx / B;
+  }
   const int base = cu[b];
   const int N = cu[b + 1] - base;
   if (kblk * kKBlock >= N) return;
@@ -340,6 +369,40 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   }
 }
 
+// List of the live 256-row blocks, (prompt, block) with the block index descending and the
+// prompt ascending within a block index, then (-1, 0) up to n_bound.  One workgroup: per block
+// index, a scan over the prompts places the prompts that reach it.  Writes stop at n_bound, so a
+// max_seqlen below the longest prompt (invalid input) stays inside the workspace.
+__global__ __launch_bounds__(1024) void block_list_kernel(const int* __restrict__ cu, int B, int nblk, int n_bound,
+                                                          int2* __restrict__ list) {
+  __shared__ int wsum[16];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int base = 0;
+  for (int k = nblk - 1; k >= 0; --k) {
+    for (int b0 = 0; b0 < B; b0 += 1024) {
+      const int b = b0 + t;
+      const int flag = (b < B && cu[b + 1] - cu[b] > k * kQBlock) ? 1 : 0;
+      int x = flag;  // inclusive scan within the wave, then over the 16 wave totals
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+      }
+      if (lane == 63) wsum[w] = x;
+      __syncthreads();
+      int before = 0, total = 0;
+      for (int i = 0; i < 16; ++i) {
+        before += (i < w) ? wsum[i] : 0;
+        total += wsum[i];
+      }
+      const int pos = base + before + x - flag;
+      if (flag && pos < n_bound) list[pos] = make_int2(b, k);
+      base += total;
+      __syncthreads();  // wsum is rewritten by the next round
+    }
+  }
+  for (int i = base + t; i < n_bound; i += 1024) list[i] = make_int2(-1, 0);
+}
+
 constexpr int kMaxWeightedLayers = 64;
 struct LayerWeights {
   float w[kMaxWeightedLayers];
@@ -366,20 +429,31 @@ __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restric
 template <int DH>
 void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
             int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S, float* lse2,
-            float* part, hipStream_t s) {
+            float* part, int2* blist, hipStream_t s) {
+  static_assert(kQBlock == kKBlock, "the two passes share one list of 256-row blocks");
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
   const int nkb = (max_seqlen + kKBlock - 1) / kKBlock;
+  // Grids sized by the longest prompt are mostly workgroups that exit at once when the lengths
+  // vary widely; then both passes run over the list of live blocks instead.
+  const size_t n_bound = block_bound(n_tok, B, max_seqlen);
+  const bool use_list = n_bound * 4 < size_t(B) * nqb * 3;
+  if (use_list) {
+    block_list_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu, B, nqb, int(n_bound), blist);
+  }
+  const int2* bl = use_list ? blist : nullptr;
+  const size_t n_rows = use_list ? n_bound : size_t(nqb) * B;  // block rows of either grid
   float lse_mul = 1.f;  // row log-sum-exps in base 2 (pass 1) ...
   if (lse_in) {         // ... or the caller's natural-log ones, converted on load
     lse2 = const_cast<float*>(lse_in);
     lse_mul = kLog2e;
   } else {
-    attn_lse_kernel<DH><<<dim3(size_t(nqb) * B * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
-                                                                                   nqb, c2, lse2);
+    attn_lse_kernel<DH><<<dim3(n_rows * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2,
+                                                                          bl, lse2);
   }
-  attn_colsum_kernel<DH><<<dim3(size_t(nkb) * B * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv,
-                                                                                    c2, lse2, lse_mul, strict, part);
+  (void)nkb;
+  attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2, lse2,
+                                                                            lse_mul, strict, bl, int(n_bound), part);
   LayerWeights lw{};
   if (layer_weights)
     for (int l = 0; l < L; ++l) lw.w[l] = layer_weights[l];
@@ -418,11 +492,11 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
 
 void launch_dh(int dh, const uint16_t* q, const uint16_t* k, const int* cu, int B, int max_seqlen, int n, int L,
                int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* lw, float* S, float* lse2,
-               float* part, hipStream_t s) {
+               float* part, int2* blist, hipStream_t s) {
   switch (dh) {
-    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
-    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
-    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, s); break;
+    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
   }
 }
 
@@ -438,6 +512,7 @@ extern "C" size_t estp_attn_importance_workspace_size(int64_t n_tok, int32_t B, 
   Carver c(nullptr);
   c.take<float>(size_t(L) * Hq * n_tok);   // lse2 [L, Hq, n_tok]
   c.take<float>(size_t(L) * Hkv * n_tok);  // column masses [L, Hkv, n_tok]
+  c.take<int2>(block_bound(n_tok, B, max_seqlen));  // list of live 256-row blocks
   return c.bytes();
 }
 
@@ -458,8 +533,9 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
   Carver c(workspace);
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, nullptr, 0, nullptr, S, lse2, part, static_cast<hipStream_t>(stream));
+            int(n_tok), L, Hq, Hkv, scale, nullptr, 0, nullptr, S, lse2, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance");
   return ESTP_OK;
 }
@@ -475,6 +551,7 @@ extern "C" size_t estp_attn_importance_from_lse_workspace_size(int64_t n_tok, in
   if (n_tok < 1 || L < 1 || Hkv < 1) return 0;
   Carver c(nullptr);
   c.take<float>(size_t(L) * Hkv * n_tok);  // column masses [L, Hkv, n_tok]
+  c.take<int2>(block_bound(n_tok, B, max_seqlen));  // list of live 256-row blocks
   return c.bytes();
 }
 
@@ -495,8 +572,9 @@ extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const
 
   Carver c(workspace);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, static_cast<hipStream_t>(stream));
+            int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance_from_lse");
   return ESTP_OK;
 }
@@ -533,9 +611,10 @@ extern "C" int estp_attn_importance_ex(const void* Q, const void* K, const float
   Carver c(workspace);
   float* lse2 = lse ? nullptr : c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
             int(n_tok), L, Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S,
-            lse2, part, static_cast<hipStream_t>(stream));
+            lse2, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance_ex");
   return ESTP_OK;
 }
