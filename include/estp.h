@@ -90,17 +90,17 @@ ESTP_API const char* estp_last_error(void);
  *
  * for every row i of X: the entropy, in nats, of the next-token distribution
  * the LM head assigns from token i's final-layer hidden state.  The logits
- * z_i (n_tok x V) never reach memory: a bf16 matrix-core GEMM streams the
- * vocabulary and keeps a running max / exp-sum / sum(p*z) per row.
+ * z_i (n_tok x V) never reach memory: a GEMM streams the vocabulary and
+ * keeps a running max / exp-sum / sum(p*z) per row (bf16 inputs: matrix
+ * cores with fp32 accumulation; fp32 inputs: fp32 FMAs throughout).
  *
  *   X  [n_tok, d]  hidden states (dtype), 16-byte aligned
  *   W  [V, d]      LM-head weight in nn.Linear layout (dtype), 16-byte aligned
  *   H  [n_tok]     float32 output
- *   dtype          ESTP_BF16 (ESTP_F32 returns ESTP_ERR_UNSUPPORTED)
- * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0; a d that is not a
- * multiple of 32 returns ESTP_ERR_UNSUPPORTED (the matrix-core k steps are
- * 32 deep), as does 512 d >= 2^32 (a 256-row tile of W must be addressable
- * with 32-bit offsets).
+ *   dtype          ESTP_BF16 or ESTP_F32 (X and W alike)
+ * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0; for ESTP_BF16 a d that is
+ * not a multiple of 32 returns ESTP_ERR_UNSUPPORTED (the matrix-core k steps
+ * are 32 deep); 512 d >= 2^32 returns it for either dtype.
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype);
 ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
@@ -125,7 +125,8 @@ ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int
  *   cu_seqlens [B+1]        int32, device
  *   scale                   score scale, typically 1/sqrt(dh); finite, > 0
  *   S  [n_tok]              float32 output
- *   dtype                   ESTP_BF16
+ *   dtype                   ESTP_BF16 (matrix-core scores, fp32 accumulation) or
+ *                           ESTP_F32 (fp32 FMAs throughout); Q and K alike
  * Requires Hq % Hkv == 0, dh in {32, 64, 128}, 1 <= max_seqlen.
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_attn_importance_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L, int32_t Hq,

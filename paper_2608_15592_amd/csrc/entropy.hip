@@ -36,6 +36,7 @@
 // XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices that
 // hold one tile more than the others are spread over the XCDs.
 #include "estp_common.h"
+#include "f32_paths.h"
 
 namespace estp {
 namespace detail {
@@ -474,8 +475,7 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
                "estp_token_entropy: d must be a positive multiple of 8, got %d", d);
   ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG,
                "estp_token_entropy: unknown dtype %d", dtype);
-  ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED, "estp_token_entropy: only ESTP_BF16 inputs are supported");
-  ESTP_REQUIRE(d % 32 == 0, ESTP_ERR_UNSUPPORTED,
+  ESTP_REQUIRE(dtype == ESTP_F32 || d % 32 == 0, ESTP_ERR_UNSUPPORTED,
                "estp_token_entropy: d must be a multiple of 32 for the matrix-core path, got %d", d);
   ESTP_REQUIRE(size_t(d) * 2 * kBV < (size_t(1) << 32), ESTP_ERR_UNSUPPORTED,
                "estp_token_entropy: d = %d too large", d);
@@ -497,6 +497,14 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pt = c.take<float>(size_t(n_vsplit) * n);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
+  if (dtype == ESTP_F32) {
+    launch_entropy_f32(static_cast<const float*>(X), static_cast<const float*>(W), n, int(d), int(V), n_vsplit, pm,
+                       ps, pt, s);
+    ESTP_CHECK_LAUNCH("entropy_f32_kernel");
+    entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
+    ESTP_CHECK_LAUNCH("entropy_merge_kernel");
+    return ESTP_OK;
+  }
   const dim3 grid(n_vsplit * n_tt), block(kWaves * 64);
   const uint16_t* Xh = static_cast<const uint16_t*>(X);
   const uint16_t* Wh = static_cast<const uint16_t*>(W);

@@ -23,6 +23,7 @@
 // SIMD (168 VGPRs, no spills) so that one wave's exponentials overlap the
 // others' matrix-core work.
 #include "estp_common.h"
+#include "f32_paths.h"
 
 namespace estp {
 namespace detail {
@@ -427,13 +428,12 @@ __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restric
 }
 
 template <int DH>
-void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
+void launch(const void* Qv, const void* Kv, bool f32, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
             int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S, float* lse2,
             float* part, int2* blist, hipStream_t s) {
   static_assert(kQBlock == kKBlock, "the two passes share one list of 256-row blocks");
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
-  const int nkb = (max_seqlen + kKBlock - 1) / kKBlock;
   // Grids sized by the longest prompt are mostly workgroups that exit at once when the lengths
   // vary widely; then both passes run over the list of live blocks instead.
   const size_t n_bound = block_bound(n_tok, B, max_seqlen);
@@ -447,13 +447,20 @@ void launch(const uint16_t* Q, const uint16_t* K, const int* cu, int B, int max_
   if (lse_in) {         // ... or the caller's natural-log ones, converted on load
     lse2 = const_cast<float*>(lse_in);
     lse_mul = kLog2e;
-  } else {
-    attn_lse_kernel<DH><<<dim3(n_rows * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2,
-                                                                          bl, lse2);
   }
-  (void)nkb;
-  attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2, lse2,
-                                                                            lse_mul, strict, bl, int(n_bound), part);
+  if (f32) {
+    launch_importance_f32(DH, static_cast<const float*>(Qv), static_cast<const float*>(Kv), cu, B, n_tok, L, Hq, Hkv,
+                          nqb, c2, bl, n_rows, int(n_bound), lse_in == nullptr, lse2, lse_mul, strict, part, s);
+  } else {
+    const uint16_t* Q = static_cast<const uint16_t*>(Qv);
+    const uint16_t* K = static_cast<const uint16_t*>(Kv);
+    if (!lse_in)
+      attn_lse_kernel<DH><<<dim3(n_rows * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2,
+                                                                            bl, lse2);
+    attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2,
+                                                                              lse2, lse_mul, strict, bl, int(n_bound),
+                                                                              part);
+  }
   LayerWeights lw{};
   if (layer_weights)
     for (int l = 0; l < L; ++l) lw.w[l] = layer_weights[l];
@@ -482,7 +489,6 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
   ESTP_REQUIRE(Hq % Hkv == 0, ESTP_ERR_INVALID_ARG, "%s: Hq (%d) must be a multiple of Hkv (%d)", fn, Hq, Hkv);
   ESTP_REQUIRE(scale > 0.f && scale < INFINITY, ESTP_ERR_INVALID_ARG, "%s: scale must be finite and > 0", fn);
   ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG, "%s: unknown dtype %d", fn, dtype);
-  ESTP_REQUIRE(dtype == ESTP_BF16, ESTP_ERR_UNSUPPORTED, "%s: only ESTP_BF16 inputs are supported", fn);
   ESTP_REQUIRE(dh == 32 || dh == 64 || dh == 128, ESTP_ERR_UNSUPPORTED, "%s: head_dim %d unsupported (32, 64, 128)",
                fn, dh);
   ESTP_REQUIRE(aligned(Q, 16) && aligned(K, 16), ESTP_ERR_INVALID_ARG, "%s: Q and K must be 16-byte aligned", fn);
@@ -490,13 +496,13 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
   return ESTP_OK;
 }
 
-void launch_dh(int dh, const uint16_t* q, const uint16_t* k, const int* cu, int B, int max_seqlen, int n, int L,
+void launch_dh(int dh, const void* q, const void* k, bool f32, const int* cu, int B, int max_seqlen, int n, int L,
                int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* lw, float* S, float* lse2,
                float* part, int2* blist, hipStream_t s) {
   switch (dh) {
-    case 32: launch<32>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
-    case 64: launch<64>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
-    default: launch<128>(q, k, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    case 32: launch<32>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    case 64: launch<64>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    default: launch<128>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
   }
 }
 
@@ -534,7 +540,7 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
             int(n_tok), L, Hq, Hkv, scale, nullptr, 0, nullptr, S, lse2, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance");
   return ESTP_OK;
@@ -573,7 +579,7 @@ extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const
   Carver c(workspace);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
             int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance_from_lse");
   return ESTP_OK;
@@ -612,7 +618,7 @@ extern "C" int estp_attn_importance_ex(const void* Q, const void* K, const float
   float* lse2 = lse ? nullptr : c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K), cu_seqlens, B, max_seqlen,
+  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
             int(n_tok), L, Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S,
             lse2, part, blist, static_cast<hipStream_t>(stream));
   ESTP_CHECK_LAUNCH("estp_attn_importance_ex");

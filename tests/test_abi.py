@@ -58,8 +58,8 @@ def test_entropy_validation():
         ((FAKE, FAKE, 100, 60, 1000, 0, FAKE, WS, ws, None), 1),        # d % 8
         ((FAKE, FAKE, 100, 64, 0, 0, FAKE, WS, ws, None), 1),           # V < 1
         ((FAKE, FAKE, 100, 64, 1000, 7, FAKE, WS, ws, None), 1),        # unknown dtype
-        ((FAKE, FAKE, 100, 64, 1000, 1, FAKE, WS, ws, None), 2),        # f32 unsupported
-        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, WS, ws, None), 2),        # d not a multiple of 32
+        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, WS, ws, None), 2),        # bf16: d not a multiple of 32
+        ((FAKE, FAKE, 100, 40, 1000, 1, FAKE, WS, ws - 1, None), 3),    # f32 takes any d % 8 == 0
         ((UNALIGNED, FAKE, 100, 64, 1000, 0, FAKE, WS, ws, None), 1),   # alignment
         ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, WS, ws - 1, None), 3),    # workspace short
         ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, None, ws, None), 1),      # workspace null
@@ -90,7 +90,7 @@ def test_importance_validation():
     assert call(scale=float("inf")) == 1
     assert call(max_seqlen=101) == 1      # longer than n_tok
     assert call(dh=96) == 2
-    assert call(dtype=1) == 2
+    assert call(dtype=1, wsb=ws - 1) == 3  # f32 accepted, then the workspace check
     assert call(wsb=ws - 1) == 3
     assert call(Q=UNALIGNED) == 1
 
@@ -115,7 +115,7 @@ def test_importance_from_lse_validation():
     assert call(Hq=5) == 1
     assert call(scale=-1.0) == 1
     assert call(dh=96) == 2
-    assert call(dtype=1) == 2
+    assert call(dtype=1, wsb=ws - 1) == 3  # f32 accepted, then the workspace check
     assert call(wsb=ws - 1) == 3
     assert call(Q=UNALIGNED) == 1
 

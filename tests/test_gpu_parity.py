@@ -100,9 +100,9 @@ def test_entropy_repeatable_bitwise():
     assert torch.equal(a, b)
 
 
-def test_entropy_rejects_f32():
-    X = torch.zeros(4, 64, device="cuda")
-    W = torch.zeros(10, 64, device="cuda")
+def test_entropy_rejects_bf16_width_not_multiple_of_32():
+    X = torch.zeros(4, 40, device="cuda", dtype=torch.bfloat16)
+    W = torch.zeros(10, 40, device="cuda", dtype=torch.bfloat16)
     with pytest.raises(estp.EstpError) as ei:
         estp.token_entropy(X, W)
     assert ei.value.status == 2
