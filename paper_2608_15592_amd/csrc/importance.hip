@@ -77,7 +77,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
                                                             const uint16_t* __restrict__ K,
                                                             const int* __restrict__ cu, int B, int n_tok,
                                                             int L, int Hq, int Hkv, int nqb_max, float c2,
-                                                            const int2* __restrict__ blist,
+                                                            const int2* __restrict__ blist, int xcd_groups,
                                                             float* __restrict__ lse2) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
@@ -88,8 +88,21 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
   // or, when many prompts are much shorter than the longest, the entry of the list of live
   // 256-row blocks (already heaviest first)
   int idx = blockIdx.x;
-  const int lh = idx % (L * Hq);
-  idx /= L * Hq;
+  int lh;
+  if (xcd_groups) {
+    // Workgroups are dealt to the 8 XCDs in turn (block id mod 8), each with its own L2. The G
+    // query heads of one KV group read the same key tiles in the same order, so ids 8s + x for
+    // s = G u', ..., G u' + G - 1 (one XCD, back to back) take the G heads of unit u = 8 u' + x,
+    // where units (block row, layer, KV head) keep the order of the plain grid.
+    const int G = Hq / Hkv;
+    const int x = idx & 7, sx = idx >> 3;
+    const int u = (sx / G) * 8 + x;
+    lh = (u % (L * Hkv)) * G + sx % G;
+    idx = u / (L * Hkv);
+  } else {
+    lh = idx % (L * Hq);
+    idx /= L * Hq;
+  }
   int b, qblk;
   if (blist) {
     const int2 e = blist[idx];
@@ -454,9 +467,13 @@ void launch(const void* Qv, const void* Kv, bool f32, const int* cu, int B, int 
   } else {
     const uint16_t* Q = static_cast<const uint16_t*>(Qv);
     const uint16_t* K = static_cast<const uint16_t*>(Kv);
+    // GQA groups on one XCD when the grid splits into whole groups per XCD
+    const size_t n_wg = n_rows * L * Hq;
+    const int G = Hq / Hkv;
+    const int xcd_groups = (G > 1 && n_wg % (size_t(8) * G) == 0) ? 1 : 0;
     if (!lse_in)
-      attn_lse_kernel<DH><<<dim3(n_rows * L * Hq), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2,
-                                                                            bl, lse2);
+      attn_lse_kernel<DH><<<dim3(n_wg), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2, bl,
+                                                                 xcd_groups, lse2);
     attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2,
                                                                               lse2, lse_mul, strict, bl, int(n_bound),
                                                                               part);
