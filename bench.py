@@ -26,6 +26,7 @@ if ROOT not in sys.path:
 METRIC = "prompt tokens/sec scored+pooled on 1 MI355X; % bf16 MFMA peak; pooling HBM GB/s"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector peak (256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz)
+PEAK_EXP_PER_S = 256 * 4 * 16 / 4 * 2.4e9  # v_exp_f32 at a quarter of the FMA issue rate: 9.83e12 per s
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 
 
@@ -349,6 +350,7 @@ def main() -> int:
 
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
+    imp_exps = 2.0 * float(sum(int(T) * (int(T) + 1) // 2 for T in inp["lengths"])) * w.Hq * w.L  # two passes
     pool_bytes = n_tok * w.d * 2 + n_tok * 4 + B * w.d * 4
     ent_tflops = ent_flop / (ent_ms * 1e-3) / 1e12
     pool_gbps = pool_bytes / (pool_ms * 1e-3) / 1e9
@@ -397,7 +399,12 @@ def main() -> int:
         "kernels_ms_median": dict(zip(("token_entropy", "attn_importance", "combine_pool", "predict"),
                                       (float(v) for v in med_ms))),
         "importance": {"alg_flop": imp_flop_alg, "alg_tflops": imp_flop_alg / (imp_ms * 1e-3) / 1e12,
-                       "executed_tflops": 2 * imp_flop_alg / (imp_ms * 1e-3) / 1e12},
+                       "executed_tflops": 2 * imp_flop_alg / (imp_ms * 1e-3) / 1e12,
+                       # each causal score is exponentiated once per pass; v_exp_f32 issues at a quarter of
+                       # the FMA rate: 256 CUs x 4 SIMDs x 16 lanes / 4 x 2.4 GHz
+                       "exp_roofline": {"bound": "alu", "exps": imp_exps, "achieved": imp_exps / (imp_ms * 1e-3),
+                                        "peak": PEAK_EXP_PER_S, "unit": "exp/s",
+                                        "frac": imp_exps / (imp_ms * 1e-3) / PEAK_EXP_PER_S}},
         "importance_from_prefill_lse": {"ms": lse_ms, "vs_two_pass": lse_ms / imp_ms,
                                         "note": "estp_attn_importance_from_lse with given row LSEs; not part of "
                                                 "the timed step"},
