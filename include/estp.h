@@ -26,7 +26,8 @@
  *    stream) and returns.  Results are visible after the caller synchronises
  *    the stream.  Calls on one stream run in order.
  *  - Argument validation happens before any device work: a failed check
- *    returns an error and enqueues nothing.  Device-resident values
+ *    returns an error and enqueues nothing.  Shapes whose kernel grid would
+ *    exceed one launch (2^32 - 1 work-items) return ESTP_ERR_UNSUPPORTED.  Device-resident values
  *    (cu_seqlens contents, NaN/Inf in tensors) are not inspected; a prompt of
  *    length 0 or a cu_seqlens array that is not non-decreasing from 0 to
  *    n_tok is invalid input with undefined results.  NaN/Inf propagate.

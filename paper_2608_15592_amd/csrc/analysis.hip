@@ -170,6 +170,8 @@ extern "C" int estp_misalignment(const float* H, const float* S, const int32_t* 
   ESTP_REQUIRE(B >= 1, ESTP_ERR_INVALID_ARG, "estp_misalignment: B must be >= 1");
   ESTP_REQUIRE(frac_low >= 0.f && frac_low <= 1.f && frac_high >= 0.f && frac_high <= 1.f, ESTP_ERR_INVALID_ARG,
                "estp_misalignment: fractions must be in [0, 1]");
+  ESTP_REQUIRE(fits_launch(size_t(B), kAThreads), ESTP_ERR_UNSUPPORTED,
+               "estp_misalignment: B = %d is more than one launch holds", B);
   misalignment_kernel<<<dim3(B), dim3(kAThreads), 0, static_cast<hipStream_t>(stream)>>>(H, S, cu_seqlens, frac_low,
                                                                                          frac_high, counts);
   ESTP_CHECK_LAUNCH("misalignment_kernel");

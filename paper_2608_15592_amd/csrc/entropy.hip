@@ -491,6 +491,9 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   const int n_vt = (V + kBV - 1) / kBV;
   const int n_tt = (n + kBT - 1) / kBT;
   const int n_vsplit = choose_vsplit(n_vt);
+  const size_t n_wg = dtype == ESTP_F32 ? entropy_f32_workgroups(n, n_vsplit) : size_t(n_vsplit) * n_tt;
+  ESTP_REQUIRE(fits_launch(n_wg, kWaves * 64), ESTP_ERR_UNSUPPORTED,
+               "estp_token_entropy: n_tok = %d needs %zu workgroups, more than one launch holds", n, n_wg);
   Carver c(workspace);
   float* pm = c.take<float>(size_t(n_vsplit) * n);
   float* ps = c.take<float>(size_t(n_vsplit) * n);

@@ -175,6 +175,10 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
   }
 }
 
+size_t entropy_f32_workgroups(int n_tok, int n_vsplit) {
+  return size_t(n_vsplit) * size_t((n_tok + kFT - 1) / kFT);
+}
+
 void launch_entropy_f32(const float* X, const float* W, int n_tok, int d, int V, int n_vsplit, float* part_m,
                         float* part_s, float* part_t, hipStream_t s) {
   const int n_vt = (V + kFV - 1) / kFV;

@@ -138,6 +138,11 @@ int current_device_cu_count();
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// A launch covers at most 2^32 - 1 work-items along its x dimension.
+inline bool fits_launch(size_t workgroups, size_t threads) {
+  return workgroups >= 1 && workgroups <= size_t(UINT32_MAX) / threads;
+}
+
 // Sequential carving of a caller workspace into 256-byte aligned pieces.
 struct Carver {
   char* base;

@@ -11,6 +11,8 @@
 namespace estp {
 namespace detail {
 
+// Workgroups in launch_entropy_f32's grid.
+size_t entropy_f32_workgroups(int n_tok, int n_vsplit);
 // Per-slice online-softmax partial states (part_m/s/t [n_vsplit, n_tok], base
 // 2) of the logits W x for every token; 1 <= n_vsplit <= ceil(V / 128).
 void launch_entropy_f32(const float* X, const float* W, int n_tok, int d, int V, int n_vsplit, float* part_m,

@@ -44,6 +44,19 @@ inline size_t block_bound(int64_t n_tok, int32_t B, int32_t max_seqlen) {
   return a < c ? a : c;
 }
 
+// Grids sized by the longest prompt are mostly workgroups that exit at once when the lengths
+// vary widely; then both passes run over the list of live blocks instead.
+inline bool use_block_list(int64_t n_tok, int32_t B, int32_t max_seqlen) {
+  const size_t nqb = (size_t(max_seqlen) + kQBlock - 1) / kQBlock;
+  return block_bound(n_tok, B, max_seqlen) * 4 < size_t(B) * nqb * 3;
+}
+
+// 256-row block entries of either grid (rows of the pass grids)
+inline size_t block_rows(int64_t n_tok, int32_t B, int32_t max_seqlen) {
+  const size_t nqb = (size_t(max_seqlen) + kQBlock - 1) / kQBlock;
+  return use_block_list(n_tok, B, max_seqlen) ? block_bound(n_tok, B, max_seqlen) : size_t(B) * nqb;
+}
+
 // Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
 // consecutive rows read at one logical chunk hit 16 distinct bank groups.
 template <int DH>
@@ -447,10 +460,8 @@ void launch(const void* Qv, const void* Kv, bool f32, const int* cu, int B, int 
   static_assert(kQBlock == kKBlock, "the two passes share one list of 256-row blocks");
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
-  // Grids sized by the longest prompt are mostly workgroups that exit at once when the lengths
-  // vary widely; then both passes run over the list of live blocks instead.
   const size_t n_bound = block_bound(n_tok, B, max_seqlen);
-  const bool use_list = n_bound * 4 < size_t(B) * nqb * 3;
+  const bool use_list = use_block_list(n_tok, B, max_seqlen);
   if (use_list) {
     block_list_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu, B, nqb, int(n_bound), blist);
   }
@@ -510,6 +521,10 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
                fn, dh);
   ESTP_REQUIRE(aligned(Q, 16) && aligned(K, 16), ESTP_ERR_INVALID_ARG, "%s: Q and K must be 16-byte aligned", fn);
   ESTP_REQUIRE(size_t(L) * Hq * n_tok < (size_t(1) << 40), ESTP_ERR_INVALID_ARG, "%s: too large", fn);
+  // the largest pass grid: pass 1 of the fp32 kernels, two workgroups per (block, layer, head)
+  ESTP_REQUIRE(fits_launch(2 * block_rows(n_tok, B, max_seqlen) * L * Hq, kThreads) &&
+                   fits_launch(size_t(B), 1) && fits_launch((size_t(max_seqlen) + 255) / 256, 256),
+               ESTP_ERR_UNSUPPORTED, "%s: batch too large for one launch", fn);
   return ESTP_OK;
 }
 

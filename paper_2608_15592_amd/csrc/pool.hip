@@ -588,8 +588,10 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
   const size_t n_k = use_map ? n_bound : size_t(B) * nch;
   const int ne = e ? (max_seqlen + kThreads - 1) / kThreads : 0;
   const int n_finish = nslices + ne;
-  ESTP_REQUIRE(n_k * nslices <= INT32_MAX && size_t(n_finish) * B <= INT32_MAX, ESTP_ERR_UNSUPPORTED,
-               "estp_combine_pool: batch too large for one launch");
+  ESTP_REQUIRE(fits_launch(n_k * nslices, kThreads) && fits_launch(size_t(n_finish) * B, kThreads) &&
+                   fits_launch(size_t(B) * ((size_t(d) + kPromptSlice - 1) / kPromptSlice), kPromptThreads) &&
+                   fits_launch(size_t(B), 1024),
+               ESTP_ERR_UNSUPPORTED, "estp_combine_pool: batch too large for one launch");
   Carver c(workspace);
   float4* coef = c.take<float4>(size_t(B));
   ChunkStat* cstat = c.take<ChunkStat>(size_t(B) * nch);
@@ -609,7 +611,7 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
   }
   if (use_prompt_path(n_tok, B, max_seqlen, d)) {
     const int ns = (d + kPromptSlice - 1) / kPromptSlice;
-    const dim3 pgrid(unsigned(B * ns));
+    const dim3 pgrid(unsigned(size_t(B) * ns));
     if (dtype == ESTP_BF16) {
       pool_prompt_kernel<uint16_t><<<pgrid, dim3(kPromptThreads), 0, s>>>(
           static_cast<const uint16_t*>(X), S, H, cu_seqlens, int(d), ns, a1, a2, cf, pooled, e, top);

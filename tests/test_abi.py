@@ -247,3 +247,22 @@ def test_analysis_validation():
     assert lib.estp_misalignment(FAKE, FAKE, FAKE, 2, 1.5, 0.4, FAKE, None) == 1
     assert lib.estp_sjf_padding(None, None, 4, 2, FAKE, None) == 1
     assert lib.estp_sjf_padding(FAKE, None, 4, 0, FAKE, None) == 1
+
+
+@needs_no_gpu
+def test_launch_size_limits():
+    # shapes whose grids would pass 2^32 work-items are refused before any device work
+    lib = estp.load()
+    n = 300_000_000  # bf16 entropy: 16 slices x ceil(n / 256) workgroups of 256 threads
+    ws = lib.estp_token_entropy_workspace_size(n, 32, 4096, 0)
+    assert lib.estp_token_entropy(FAKE, FAKE, n, 32, 4096, 0, FAKE, WS, ws, None) == 2
+    assert b"launch" in lib.estp_last_error()
+    n = 2_000_000_000  # importance: 2 x (n / 256) x L x Hq fp32 pass-1 workgroups
+    ws = lib.estp_attn_importance_workspace_size(n, 1, n, 1, 2, 2, 64, 0)
+    assert lib.estp_attn_importance(FAKE, FAKE, FAKE, 1, n, n, 1, 2, 2, 64, 0.125, 0, FAKE, WS, ws, None) == 2
+    assert b"launch" in lib.estp_last_error()
+    B, T, d = (1 << 20) - 1, 2048, 8192  # pooling: B x d / 512 one-kernel workgroups of 512 threads
+    ws = lib.estp_combine_pool_workspace_size(B * T, B, T, d, 0)
+    args = [FAKE, FAKE, FAKE, FAKE, B, T, B * T, d, 0.5, 0.5, 1.0, 0, 0, FAKE, None, None, WS, ws, None]
+    assert lib.estp_combine_pool(*args) == 2
+    assert b"launch" in lib.estp_last_error()
