@@ -192,8 +192,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build targets one GPU: the path is measured on one MI355X; "
-                                   "run with --gpus 1 (multi-GPU sharding is described in DESIGN.md only)"}))
+        print(json.dumps({"error": "the path runs on one GPU: it is measured on one MI355X and has no "
+                                   "multi-GPU sharding; run with --gpus 1"}))
         return 2
 
     import torch
