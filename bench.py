@@ -186,6 +186,7 @@ def main() -> int:
     ap.add_argument("--alpha", type=float, default=1.0)
     ap.add_argument("--norm", default="none", choices=["none", "zscore", "minmax"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true", help="also time the step captured in a HIP graph")
     ap.add_argument("--cpu-sample-prompts", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run 3 device-to-device copies of BYTES (calibrates HBM byte counters)")
@@ -232,23 +233,23 @@ def main() -> int:
     bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, n_bins, X.device)
     stream = torch.cuda.current_stream()
 
-    def step(evs=None):
+    def step(evs=None, s=stream):
         if evs:
-            evs[0].record(stream)
-        H = estp.token_entropy(X, W, H=bufs["H"], workspace=bufs["ws_entropy"], stream=stream)
+            evs[0].record(s)
+        H = estp.token_entropy(X, W, H=bufs["H"], workspace=bufs["ws_entropy"], stream=s)
         if evs:
-            evs[1].record(stream)
-        S = estp.attn_importance(Q, K, cu, max_len, S=bufs["S"], workspace=bufs["ws_importance"], stream=stream)
+            evs[1].record(s)
+        S = estp.attn_importance(Q, K, cu, max_len, S=bufs["S"], workspace=bufs["ws_importance"], stream=s)
         if evs:
-            evs[2].record(stream)
+            evs[2].record(s)
         pooled, _, _ = estp.combine_pool(X, S, H, cu, max_len, args.lambda1, args.lambda2, args.alpha, args.norm,
                                          pooled=bufs["pooled"], e=bufs["e"], top=bufs["top"],
-                                         workspace=bufs["ws_pool"], stream=stream)
+                                         workspace=bufs["ws_pool"], stream=s)
         if evs:
-            evs[3].record(stream)
-        estp.predict(pooled, *head, workspace=bufs["ws_predict"], stream=stream)
+            evs[3].record(s)
+        estp.predict(pooled, *head, workspace=bufs["ws_predict"], stream=s)
         if evs:
-            evs[4].record(stream)
+            evs[4].record(s)
 
     for i in range(args.warmup):
         step()
@@ -270,6 +271,34 @@ def main() -> int:
     med_ms = np.median(per_call, axis=0)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step "
         f"(entropy {ent_ms:.3f}, importance {imp_ms:.3f}, combine+pool {pool_ms:.3f}, head {pred_ms:.3f} ms)")
+
+    # Side measurement: the same step captured once in a HIP graph and replayed (no launch gaps).
+    graph_info = None
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):  # warm-up off the default stream before capture
+            step(s=side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(s=torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        g0, g1 = HipEvent(), HipEvent()
+        g0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        gms = g0.elapsed_time(g1) / args.steps
+        graph_info = {"ms_per_step": gms, "tokens_per_s": n_tok / (gms * 1e-3), "eager_over_graph": ms_per_step / gms,
+                      "note": "the timed step captured once in a HIP graph and replayed; not part of value"}
+        del g
+        log(f"graph replay: {gms:.3f} ms/step (eager {ms_per_step:.3f})")
 
     # The one-pass importance call fed with a prefill's row log-sum-exps (here formed with plain
     # fp32 torch, untimed); timed on its own, outside the step.
@@ -419,6 +448,7 @@ def main() -> int:
                             "resident (importance streams 2.7 GB of Q and K just before); device copy counts "
                             "read + write bytes"},
         "device": torch.cuda.get_device_name(0),
+        **({"graph": graph_info} if graph_info else {}),
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host sample ...")
