@@ -55,16 +55,21 @@ def cpu_baseline(inp, lam1, lam2, alpha, norm, n_prompts: int):
     n = int(cu[n_prompts])
     cu_s = cu[: n_prompts + 1]
     t0 = time.perf_counter()
-    out = oracle.run_path(inp["X"][:n], inp["W"], inp["Q"][:, :n], inp["K"][:, :n], cu_s, lam1, lam2, alpha, norm,
-                          head=(inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"]))
-    dt = time.perf_counter() - t0
-    del out
+    reps = 0
+    while True:  # a sample that runs in well under a second is repeated, for a stable rate
+        oracle.run_path(inp["X"][:n], inp["W"], inp["Q"][:, :n], inp["K"][:, :n], cu_s, lam1, lam2, alpha, norm,
+                        head=(inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"]))
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= 2.0:
+            break
     return {
-        "value": n / dt,
+        "value": reps * n / dt,
         "unit": "tokens/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": f"the first {n_prompts} whole prompts of the workload ({n} tokens), whole path, {dt:.1f} s",
+        "sample": (f"the first {n_prompts} whole prompts of the workload ({n} tokens), whole path"
+                   + (f", {reps} times" if reps > 1 else "") + f", {dt:.1f} s"),
         "host_cpus": len(os.sched_getaffinity(0)),
     }
 
