@@ -421,12 +421,12 @@ def main() -> int:
             "traffic": recorded_traffic(args.workload),
             "work_per_launch": f"2*n_tok*V*d = {ent_flop:.4g} FLOP",
             # from the committed GRBM_GUI_ACTIVE / SQ_VALU_MFMA_BUSY_CYCLES summary of this kernel source
-            "sustained_clock_GHz": clock[0] if clock else None,
-            "frac_at_sustained_clock": ent_tflops / (PEAK_BF16_TFLOPS * clock[0] / 2.4) if clock else None,
-            "mfma_busy": clock[1] if clock else None,
+            "counter_run_clock_GHz": clock[0] if clock else None,
+            "counter_run_mfma_busy": clock[1] if clock else None,
             "clock_note": "core clock and matrix-pipe busy of this kernel from GRBM_GUI_ACTIVE and "
-                          "SQ_VALU_MFMA_BUSY_CYCLES in a separate counter run (profiles/); the chip is power-limited "
-                          "under this load, and the nominal peak assumes 2.4 GHz",
+                          "SQ_VALU_MFMA_BUSY_CYCLES in a separate counter run (profiles/), possibly on another box: "
+                          "boxes differ by up to ~6% in the clock they sustain. The chip is power-limited under this "
+                          "load, and the nominal peak assumes 2.4 GHz",
         },
         "kernels_ms": {"token_entropy": ent_ms, "attn_importance": imp_ms, "combine_pool": pool_ms,
                        "predict": pred_ms},
