@@ -8,9 +8,12 @@ library against plain, slow definitions.  It shares no code with the HIP path.
 Every function takes bf16 bit patterns (uint16) or float arrays, widens them
 exactly to float64 and evaluates the paper's definitions:
 
-* ``token_entropy``      - Eq. 2 (Section 4.2)
+* ``token_entropy``      - Eq. 2 (Section 4.2); ``vocab_argmax`` - the mode of
+  the same next-token distribution (largest logit, lowest index among ties)
 * ``attn_importance``    - Eq. 1 (Section 4.1); ``attn_importance_tail``
-  gives the same S_j for the last m keys of one prompt from its last m rows;
+  gives the same S_j for the last m keys of one prompt from its last m rows,
+  ``attn_importance_keys`` for any set of keys of one prompt from the rows
+  that reach them;
   ``attn_row_lse`` is the log normaliser of every attention row and
   ``attn_importance_from_lse`` forms S_j from given row normalisers
 * ``combine_weights``    - Eq. 3 and Eq. 4 (Section 4.2)
@@ -29,8 +32,10 @@ and against invariants the definitions fix.
 from .estp_oracle import (  # noqa: F401
     widen,
     token_entropy,
+    vocab_argmax,
     attn_importance,
     attn_importance_tail,
+    attn_importance_keys,
     attn_row_lse,
     attn_importance_from_lse,
     combine_weights,

@@ -69,6 +69,26 @@ def token_entropy(X, W, row_chunk: Optional[int] = None) -> np.ndarray:
     return H
 
 
+def vocab_argmax(X, W, row_chunk: Optional[int] = None) -> np.ndarray:
+    """Most probable next token of each row under Eq. 2's distribution (Section 4.2).
+
+    P_i = softmax(W h_i) is increasing in the logit, so the mode is the index
+    of the largest logit z_v = W[v] . h_i; among equal largest logits the
+    lowest index.  Logits are formed exactly as in ``token_entropy`` (fp64
+    products of the widened inputs).  Returns int64 [n].
+    """
+    Xd = widen(X)
+    Wd = widen(W)
+    n = Xd.shape[0]
+    if row_chunk is None:
+        row_chunk = int(max(64, min(1024, (1 << 26) // max(1, Wd.shape[0]))))
+    out = np.empty(n, dtype=np.int64)
+    for r0 in range(0, n, row_chunk):
+        z = Xd[r0:r0 + row_chunk] @ Wd.T
+        out[r0:r0 + row_chunk] = np.argmax(z, axis=1)     # first occurrence of the maximum
+    return out
+
+
 # ----------------------------------------------------------------------------- Eq. 1
 
 def _causal_softmax_rows(s: np.ndarray, i0: int) -> np.ndarray:
@@ -234,6 +254,53 @@ def attn_importance_tail(Q, K, N: int, m: int, scale: Optional[float] = None) ->
             colsum += A[:, i0:].sum(axis=0) / Hq
         S += colsum / N
     return S
+
+
+def attn_importance_keys(Q, K, N: int, keys, scale: Optional[float] = None, heads=None,
+                         row_chunk: int = 256) -> np.ndarray:
+    """S_j of Eq. 1 for the keys ``keys`` (any indices 0 <= j < N) of ONE prompt of length N.
+
+    Key j receives attention from the queries i >= j only, so every row
+    i >= min(keys) is formed in full (all of its i+1 causal scores, its own
+    softmax normaliser) and its entries at the requested keys are added to
+    their column sums.  ``Q`` [L, N, Hq, dh] and ``K`` [L, N, Hkv, dh] hold
+    that prompt alone.  ``heads`` restricts the head average of Eq. 1 to a
+    subset of the query heads (each term still divided by Hq), so that the
+    sums over a partition of the heads add up to S; default all heads.
+    Returns [len(keys)], summed over layers like ``attn_importance``.
+    """
+    Qd = widen(Q)
+    Kd = widen(K)
+    if Qd.ndim == 3:
+        Qd, Kd = Qd[None], Kd[None]
+    L, n, Hq, dh = Qd.shape
+    keys = np.asarray(keys, dtype=np.int64)
+    if n != N or keys.size == 0 or keys.min() < 0 or keys.max() >= N:
+        raise ValueError("Q, K must hold exactly the prompt and every key must lie in [0, N)")
+    G = Hq // Kd.shape[2]
+    if scale is None:
+        scale = 1.0 / math.sqrt(dh)
+    heads = range(Hq) if heads is None else heads
+    first = int(keys.min())
+    S = np.zeros(keys.size, dtype=np.float64)
+    for l in range(L):
+        colsum = np.zeros(keys.size, dtype=np.float64)
+        for h in heads:
+            for i0 in range(first, N, row_chunk):
+                i1 = min(N, i0 + row_chunk)
+                s = scale * (Qd[l, i0:i1, h, :] @ Kd[l, :i1, h // G, :].T)   # rows i0..i1-1, keys 0..i1-1
+                A = _causal_softmax_rows(s, i0)
+                colsum += _gather_cols(A, keys, i1) / Hq
+        S += colsum / N
+    return S
+
+
+def _gather_cols(A: np.ndarray, keys: np.ndarray, width: int) -> np.ndarray:
+    """Column sums of A [rows, width] at the given key indices; keys at or past ``width`` are 0."""
+    out = np.zeros(keys.size, dtype=np.float64)
+    inside = keys < width
+    out[inside] = A[:, keys[inside]].sum(axis=0)
+    return out
 
 
 # ----------------------------------------------------------------------------- Eq. 3, 4

@@ -56,6 +56,36 @@ def test_entropy_mutant_caught(name):
     assert _fails_some(P.ENTROPY_PINS, ENTROPY_MUTANTS[name]), name
 
 
+# ---------------------------------------------------------------------------- next-token mode mutants
+
+def _argmax_mutant(kind):
+    def vocab_argmax(X, W, row_chunk=None):
+        z = O.widen(X) @ O.widen(W).T
+        if kind == "last_of_ties":
+            return z.shape[1] - 1 - np.argmax(z[:, ::-1], axis=1)
+        if kind == "argmin":
+            return np.argmin(z, axis=1)
+        if kind == "off_by_one":
+            return np.argmax(z, axis=1) + 1
+        if kind == "mode_of_previous_row":
+            return np.roll(np.argmax(z, axis=1), 1)
+        if kind == "argmax_of_weight_norm":
+            return np.repeat(np.argmax(np.abs(O.widen(W)).sum(axis=1)), z.shape[0])
+        return np.argmax(z, axis=1)
+    return vocab_argmax
+
+
+@pytest.mark.parametrize("kind", ["last_of_ties", "argmin", "off_by_one", "mode_of_previous_row",
+                                  "argmax_of_weight_norm"])
+def test_argmax_mutant_caught(kind):
+    assert _fails_some(P.ARGMAX_PINS, _argmax_mutant(kind)), kind
+
+
+def test_argmax_mutant_control():
+    for pin in P.ARGMAX_PINS:
+        pin(_argmax_mutant("none"))
+
+
 # ---------------------------------------------------------------------------- importance mutants
 
 def _importance_mutant(kind):
@@ -130,7 +160,12 @@ def _combine_mutant(kind):
             lo, hi = int(cu[b]), int(cu[b + 1])
             s, h = S[lo:hi], H[lo:hi]
             if norm == "zscore":
-                s = (s - s.mean()) / (s.std() + 1e-6); h = (h - h.mean()) / (h.std() + 1e-6)
+                if kind == "zscore_ddof1":
+                    s = (s - s.mean()) / (s.std(ddof=1) + 1e-6); h = (h - h.mean()) / (h.std(ddof=1) + 1e-6)
+                elif kind == "zscore_eps_in_sqrt":
+                    s = (s - s.mean()) / np.sqrt(s.var() + 1e-6); h = (h - h.mean()) / np.sqrt(h.var() + 1e-6)
+                else:
+                    s = (s - s.mean()) / (s.std() + 1e-6); h = (h - h.mean()) / (h.std() + 1e-6)
             T = lambda1 * s + lambda2 * h
             u = {"no_alpha": T, "alpha_multiplies": T * alpha}.get(kind, T / alpha)
             w = np.exp(u - u.max())
@@ -140,9 +175,15 @@ def _combine_mutant(kind):
     return combine_weights
 
 
-@pytest.mark.parametrize("kind", ["swapped_lambdas", "batch_softmax", "no_alpha", "alpha_multiplies", "unnormalised"])
+@pytest.mark.parametrize("kind", ["swapped_lambdas", "batch_softmax", "no_alpha", "alpha_multiplies", "unnormalised",
+                                  "zscore_ddof1", "zscore_eps_in_sqrt"])
 def test_combine_mutant_caught(kind):
     assert _fails_some(P.COMBINE_PINS, _combine_mutant(kind)), kind
+
+
+def test_combine_mutant_control():
+    for pin in P.COMBINE_PINS:
+        pin(_combine_mutant("none"))
 
 
 # ---------------------------------------------------------------------------- pool and predict mutants
@@ -183,6 +224,14 @@ def _predict_mutant(kind):
             h = np.asarray(pooled, float); a = np.maximum(h @ np.asarray(W1, float).T + (0 if b1 is None else b1), 0)
             o = a @ np.asarray(W2, float).T + (0 if b2 is None else b2)
             y = o @ np.asarray(centres, float)
+        elif kind == "gelu_erf" and act == "gelu_tanh":
+            h = np.asarray(pooled, float)
+            z = h @ np.asarray(W1, float).T + (0 if b1 is None else b1)
+            a = z * 0.5 * (1.0 + np.vectorize(math.erf)(z / math.sqrt(2.0)))
+            o = a @ np.asarray(W2, float).T + (0 if b2 is None else b2)
+            if o.shape[1] == 1:
+                y = o[:, 0]
+                order = np.argsort(y, kind="stable")
         elif kind == "no_activation":
             h = np.asarray(pooled, float)
             o = (h @ np.asarray(W1, float).T + (0 if b1 is None else b1)) @ np.asarray(W2, float).T + (0 if b2 is None else b2)
@@ -192,7 +241,8 @@ def _predict_mutant(kind):
     return predict
 
 
-@pytest.mark.parametrize("kind", ["descending", "ties_reversed", "argmin_bin", "no_softmax", "no_activation"])
+@pytest.mark.parametrize("kind", ["descending", "ties_reversed", "argmin_bin", "no_softmax", "no_activation",
+                                  "gelu_erf"])
 def test_predict_mutant_caught(kind):
     assert _fails_some(P.PREDICT_PINS, _predict_mutant(kind)), kind
 
@@ -219,6 +269,32 @@ def _row_lse_excl_diag(Q, K, cu, scale=None, row_chunk=2048):
                 with np.errstate(invalid="ignore"):
                     out[l, h, lo:hi] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
     return out
+
+
+def _keys_mutant(kind):
+    def f(Q, K, N, keys, scale=None, heads=None, row_chunk=256):
+        Qd, Kd = O.widen(Q), O.widen(K)
+        if Qd.ndim == 3:
+            Qd, Kd = Qd[None], Kd[None]
+        L, n, Hq, dh = Qd.shape
+        keys = np.asarray(keys, dtype=np.int64)
+        sc = 1 / math.sqrt(dh) if scale is None else scale
+        G = Hq // Kd.shape[2]
+        first = int(keys.max()) if kind == "rows_from_last_key" else int(keys.min())
+        S = np.zeros(keys.size)
+        for l in range(L):
+            for h in (range(Hq) if heads is None else heads):
+                for i0 in range(first, N, row_chunk):
+                    i1 = min(N, i0 + row_chunk)
+                    s = sc * Qd[l, i0:i1, h] @ Kd[l, :i1, h // G].T
+                    if kind != "not_causal_in_chunk":
+                        s = np.where(np.arange(i1)[None, :] <= np.arange(i0, i1)[:, None], s, -np.inf)
+                    A = np.exp(s - s.max(axis=1, keepdims=True)); A /= A.sum(axis=1, keepdims=True)
+                    inside = keys < i1
+                    S[inside] += A[:, keys[inside]].sum(axis=0) / Hq
+        norm = (N - keys) if kind == "per_key_count" else N
+        return S / norm
+    return f
 
 
 def _head_mutant(kind):
@@ -311,6 +387,14 @@ LATER_MUTANTS = {
                                    layer_weights=None: O.attn_importance(Q, K, cu, scale, exclude_self=exclude_self,
                                                                          layer_weights=layer_weights),
                                    [P.test_importance_from_lse_bruteforce_and_identity]),
+    "keys_rows_from_last_key": ("attn_importance_keys", _keys_mutant("rows_from_last_key"),
+                                [P.test_importance_keys_match_whole_prompt, P.test_importance_keys_harmonic_and_bruteforce]),
+    "keys_rows_not_causal_in_chunk": ("attn_importance_keys", _keys_mutant("not_causal_in_chunk"),
+                                      [P.test_importance_keys_match_whole_prompt,
+                                       P.test_importance_keys_harmonic_and_bruteforce]),
+    "keys_normaliser_per_key_count": ("attn_importance_keys", _keys_mutant("per_key_count"),
+                                      [P.test_importance_keys_match_whole_prompt,
+                                       P.test_importance_keys_harmonic_and_bruteforce]),
     "head_mse_grad_sign": ("head_loss_and_grads", _head_mutant("mse_grad_sign"),
                            [lambda: P.test_head_gradients_match_finite_differences("relu")]),
     "head_no_batch_mean": ("head_loss_and_grads", _head_mutant("no_batch_mean"),

@@ -25,7 +25,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json
 
 def _ev(v):
     if isinstance(v, str):
-        return float(eval(v, {"log": math.log, "Fraction": Fraction, "exp": math.exp}))
+        return float(eval(v, {"log": math.log, "Fraction": Fraction, "exp": math.exp, "sqrt": math.sqrt}))
     if isinstance(v, list):
         return [_ev(x) for x in v]
     return float(v)
@@ -115,6 +115,53 @@ def pin_entropy_bruteforce(token_entropy):
 
 ENTROPY_PINS = [pin_entropy_uniform, pin_entropy_one_hot, pin_entropy_closed_form, pin_entropy_two_maxima,
                 pin_entropy_textbook, pin_entropy_bounds_and_invariance, pin_entropy_bruteforce]
+
+
+# ============================================================================ next-token mode (Eq. 2)
+
+def pin_argmax_one_hot(vocab_argmax):
+    # x = e_0 and one row k with a large first weight: the mode is k, wherever k is
+    V = 300
+    W = _rng(50).uniform(-1, 1, (V, 3))
+    X = np.array([[1.0, 0.0, 0.0], [1.0, 0.0, 0.0]])
+    for k in (0, 137, V - 1):
+        Wk = W.copy(); Wk[k, 0] = 10.0
+        assert list(vocab_argmax(X, Wk)) == [k, k]
+
+
+def pin_argmax_ties_lowest(vocab_argmax):
+    # equal largest logits: the lowest vocabulary index wins (also the worked example in tests/golden)
+    V = 500
+    W = _rng(51).uniform(-1, 1, (V, 2)); W[[3, 77, 400], 0] = 50.0; W[[3, 77, 400], 1] = 0.0
+    assert list(vocab_argmax(np.array([[1.0, 0.25]]), W)) == [3]
+    for ex in _golden()["vocab_argmax"]:
+        assert list(vocab_argmax(np.array(ex["X"]), np.array(ex["W"]))) == ex["argmax"]
+
+
+def pin_argmax_permutation(vocab_argmax):
+    # permuting the vocabulary rows moves the mode with them (continuous random logits: no ties)
+    X = _rng(52).standard_normal((9, 16)); W = _rng(53).standard_normal((211, 16))
+    a = vocab_argmax(X, W)
+    perm = _rng(54).permutation(211)
+    b = vocab_argmax(X, W[perm])
+    np.testing.assert_array_equal(perm[b], a)
+
+
+def pin_argmax_bruteforce(vocab_argmax):
+    # scalar loops: exact logits by fsum, first strict maximum; and the mode of scipy's softmax
+    X = _rng(55).standard_normal((5, 6)); W = _rng(56).standard_normal((40, 6))
+    got = vocab_argmax(X, W)
+    for i in range(5):
+        z = [math.fsum(W[v, k] * X[i, k] for k in range(6)) for v in range(40)]
+        best = 0
+        for v in range(1, 40):
+            if z[v] > z[best]:
+                best = v
+        assert got[i] == best
+        assert got[i] == int(np.argmax(scipy.special.softmax(np.array(z))))
+
+
+ARGMAX_PINS = [pin_argmax_one_hot, pin_argmax_ties_lowest, pin_argmax_permutation, pin_argmax_bruteforce]
 
 
 # ============================================================================ importance (Eq. 1)
@@ -262,6 +309,18 @@ def pin_combine_zscore(combine_weights):
     np.testing.assert_allclose(e3, e4, rtol=1e-12)
 
 
+def pin_combine_zscore_by_hand(combine_weights):
+    # hand-derived z-scored examples (tests/golden): population std, epsilon added to the std.
+    # Sample std (ddof 1) or epsilon inside the square root change these values by 1e-2 to 1e-1.
+    for ex in _golden()["combine_zscore"]:
+        cu = np.concatenate([[0], np.cumsum(ex["lengths"])])
+        e, top = combine_weights(np.array(ex["S"]), np.array(ex["H"]), cu, ex["lambda1"], ex["lambda2"],
+                                 ex["alpha"], norm="zscore")
+        u = np.array(_ev(ex["u"]))
+        np.testing.assert_allclose(e, np.exp(u) / np.exp(u).sum(), rtol=1e-12)
+        assert list(top) == ex["top"]
+
+
 def pin_combine_bruteforce(combine_weights):
     lengths = [3, 5]
     S = _rng(27).random(8); H = _rng(28).random(8) * 2
@@ -270,7 +329,7 @@ def pin_combine_bruteforce(combine_weights):
 
 
 COMBINE_PINS = [pin_combine_simplex_and_average, pin_combine_two_token_logistic, pin_combine_invariances,
-                pin_combine_zscore, pin_combine_bruteforce]
+                pin_combine_zscore, pin_combine_zscore_by_hand, pin_combine_bruteforce]
 
 
 # ============================================================================ pooling (Eq. 5)
@@ -347,7 +406,22 @@ def pin_predict_gelu(predict):
     assert y[2] == 0.0 and abs(y[4] - 6.0) < 1e-6
 
 
-PREDICT_PINS = [pin_predict_mlp, pin_predict_bins, pin_predict_order_stable, pin_predict_gelu]
+def pin_predict_gelu_tanh_values(predict):
+    # the tanh form of GELU at worked points (tests/golden) and against PyTorch's own
+    # gelu(approximate="tanh") in fp64 on a grid; the exact erf form misses by 1e-5 to 4e-4
+    import torch
+    ex = _golden()["predict_gelu_tanh"][0]
+    xs = np.array(ex["x"])[:, None]
+    y, _, _ = predict(xs, np.eye(1), None, np.eye(1), None, None, "gelu_tanh")
+    np.testing.assert_allclose(y, ex["yhat"], rtol=1e-12, atol=1e-15)
+    grid = np.linspace(-6.0, 6.0, 97)[:, None]
+    y, _, _ = predict(grid, np.eye(1), None, np.eye(1), None, None, "gelu_tanh")
+    ref = torch.nn.functional.gelu(torch.from_numpy(grid[:, 0].copy()), approximate="tanh").numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-15)
+
+
+PREDICT_PINS = [pin_predict_mlp, pin_predict_bins, pin_predict_order_stable, pin_predict_gelu,
+                pin_predict_gelu_tanh_values]
 
 
 # ============================================================================ runs on the oracle
@@ -355,6 +429,11 @@ PREDICT_PINS = [pin_predict_mlp, pin_predict_bins, pin_predict_order_stable, pin
 @pytest.mark.parametrize("pin", ENTROPY_PINS, ids=lambda f: f.__name__)
 def test_entropy_pins(pin):
     pin(oracle.token_entropy)
+
+
+@pytest.mark.parametrize("pin", ARGMAX_PINS, ids=lambda f: f.__name__)
+def test_argmax_pins(pin):
+    pin(oracle.vocab_argmax)
 
 
 @pytest.mark.parametrize("pin", IMPORTANCE_PINS, ids=lambda f: f.__name__)
@@ -396,6 +475,35 @@ def test_importance_tail_matches_whole_prompt():
     Q0 = np.zeros((1, N, 2, 4))
     tail = oracle.attn_importance_tail(Q0, K[:1, :, :2, :4], N, 10)
     np.testing.assert_allclose(tail, [(_harm(N) - _harm(j)) / N for j in range(N - 10, N)], rtol=1e-13)
+
+
+def test_importance_keys_match_whole_prompt():
+    # any key set of one prompt, from the rows that reach it: equal to the whole-prompt S there,
+    # to the tail form on the last keys, and the head partition sums to the full head average
+    N, L = 61, 2
+    Q = _rng(44).standard_normal((L, N, 4, 8)) * 1.5
+    K = _rng(45).standard_normal((L, N, 2, 8))
+    full = oracle.attn_importance(Q, K, [0, N])
+    for keys, chunk in (([0], 256), ([0, 1, 2, 30, 60], 7), (list(range(20, 45)), 5), ([60, 5, 33], 13)):
+        np.testing.assert_allclose(oracle.attn_importance_keys(Q, K, N, keys, row_chunk=chunk), full[keys],
+                                   rtol=1e-13)
+    np.testing.assert_allclose(oracle.attn_importance_keys(Q, K, N, range(N - 9, N)),
+                               oracle.attn_importance_tail(Q, K, N, 9), rtol=1e-13)
+    parts = sum(oracle.attn_importance_keys(Q, K, N, [0, 17], heads=[h]) for h in range(4))
+    np.testing.assert_allclose(parts, full[[0, 17]], rtol=1e-13)
+
+
+def test_importance_keys_harmonic_and_bruteforce():
+    # Q = 0: uniform causal rows, S_j = (H_N - H_j) / N on any key set; and the pure-Python brute force
+    N = 40
+    K = _rng(46).standard_normal((1, N, 1, 4))
+    got = oracle.attn_importance_keys(np.zeros((1, N, 2, 4)), K, N, [0, 7, 39], row_chunk=6)
+    np.testing.assert_allclose(got, [(_harm(N) - _harm(j)) / N for j in (0, 7, 39)], rtol=1e-13)
+    n = 7
+    Q = _rng(47).standard_normal((n, 2, 3)); Kb = _rng(48).standard_normal((n, 1, 3))
+    ref = bruteforce.importance(Q.tolist(), Kb.tolist(), [n], 0.6)
+    got = oracle.attn_importance_keys(Q, Kb, n, [1, 4, 6], scale=0.6, row_chunk=2)
+    np.testing.assert_allclose(got, [ref[1], ref[4], ref[6]], rtol=1e-13)
 
 
 def test_widen_bf16_exact():
