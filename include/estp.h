@@ -98,14 +98,21 @@ ESTP_API const char* estp_last_error(void);
  *   X  [n_tok, d]  hidden states (dtype), 16-byte aligned
  *   W  [V, d]      LM-head weight in nn.Linear layout (dtype), 16-byte aligned
  *   H  [n_tok]     float32 output
+ *   vocab_argmax [n_tok]  int32 output, or NULL: the mode of the same
+ *                  distribution, argmax_v P_i(v), i.e. the vocabulary index of
+ *                  the largest logit z_i[v] as computed here (fp32
+ *                  accumulation), the lowest index among equal largest logits.
+ *                  Unspecified for rows whose logits are not all finite.
+ *                  NULL skips the bookkeeping.
  *   dtype          ESTP_BF16 or ESTP_F32 (X and W alike)
  * Requires n_tok >= 1, V >= 1, d >= 8, d % 8 == 0; for ESTP_BF16 a d that is
  * not a multiple of 32 returns ESTP_ERR_UNSUPPORTED (the matrix-core k steps
- * are 32 deep); 512 d >= 2^32 returns it for either dtype.
+ * are 32 deep); 512 d >= 2^32 returns it for either dtype.  The workspace
+ * size does not depend on whether vocab_argmax is requested.
  * ------------------------------------------------------------------------ */
 ESTP_API size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, int32_t V, int dtype);
 ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
-                       float* H, void* workspace, size_t workspace_bytes, void* stream);
+                       float* H, int32_t* vocab_argmax, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Attention importance (Eq. 1, Section 4.1).

@@ -3,11 +3,15 @@
 Argument marshalling only: shapes and strides are read from torch tensors,
 outputs and workspaces are allocated with torch on the tensors' device, and
 every step of the computation runs in the library's HIP kernels on the
-current torch stream.  There is no fallback: if the library is missing or a
-call fails, an exception is raised.
+given stream (default: the current torch stream).  Tensors a wrapper
+allocates are allocated on that same stream, so torch's caching allocator
+never hands their memory to other work while the kernels still use it.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import math
 import os
@@ -70,7 +74,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_token_entropy_workspace_size.restype = _SZ
     lib.estp_token_entropy_workspace_size.argtypes = [_I64, _I32, _I32, _INT]
     lib.estp_token_entropy.restype = _INT
-    lib.estp_token_entropy.argtypes = [_P, _P, _I64, _I32, _I32, _INT, _P, _P, _SZ, _P]
+    lib.estp_token_entropy.argtypes = [_P, _P, _I64, _I32, _I32, _INT, _P, _P, _P, _SZ, _P]
     lib.estp_attn_importance_workspace_size.restype = _SZ
     lib.estp_attn_importance_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _I32, _I32, _I32, _INT]
     lib.estp_attn_importance.restype = _INT
@@ -126,10 +130,17 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream, device=None) -> ctypes.c_void_p:
-    if stream is None:
-        stream = torch.cuda.current_stream(device)
-    return ctypes.c_void_p(stream.cuda_stream)
+@contextlib.contextmanager
+def _on(stream, device):
+    """Make ``device`` current and ``stream`` (default: the device's current stream) the
+    current stream; yields the stream handle to pass to the library.  Every tensor a
+    wrapper allocates inside (outputs, workspace) then belongs to the stream the kernels
+    are enqueued on: when it is freed, the caching allocator reuses the block only for
+    work ordered after that stream's kernels."""
+    with torch.cuda.device(device):
+        s = torch.cuda.current_stream(device) if stream is None else stream
+        with torch.cuda.stream(s):
+            yield ctypes.c_void_p(s.cuda_stream)
 
 
 def _need(t: torch.Tensor, name: str, device=None, dtype=None, ndim=None):
@@ -169,8 +180,13 @@ def token_entropy_workspace_size(n_tok: int, d: int, V: int, dtype=torch.bfloat1
 
 
 def token_entropy(X: torch.Tensor, W: torch.Tensor, H: Optional[torch.Tensor] = None,
-                  workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """H[i] = entropy (nats) of softmax(W @ X[i]) over the vocabulary (Eq. 2)."""
+                  workspace: Optional[torch.Tensor] = None, stream=None,
+                  vocab_argmax: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """H[i] = entropy (nats) of softmax(W @ X[i]) over the vocabulary (Eq. 2).
+
+    ``vocab_argmax`` (optional int32 [n_tok] device tensor) is filled with each row's
+    most probable next token: the index of its largest logit, lowest index among ties.
+    """
     lib = load()
     _need(X, "X", ndim=2)
     _need(W, "W", device=X.device, dtype=X.dtype, ndim=2)
@@ -178,17 +194,29 @@ def token_entropy(X: torch.Tensor, W: torch.Tensor, H: Optional[torch.Tensor] = 
     V = W.shape[0]
     if W.shape[1] != d:
         raise ValueError("X and W disagree on d")
-    if H is None:
-        H = torch.empty(n_tok, dtype=torch.float32, device=X.device)
-    _need(H, "H", device=X.device, dtype=torch.float32)
-    if H.numel() != n_tok:
-        raise ValueError("H must have n_tok elements")
+    if vocab_argmax is not None:
+        _sized(vocab_argmax, "vocab_argmax", n_tok, device=X.device, dtype=torch.int32)
     dt = _dtype_code(X)
-    workspace, wsb = _workspace(lib.estp_token_entropy_workspace_size(n_tok, d, V, dt), X.device, workspace)
-    with torch.cuda.device(X.device):
-        _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(workspace), wsb,
-                                      _stream(stream, X.device)), "estp_token_entropy")
+    with _on(stream, X.device) as st:
+        if H is None:
+            H = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+        _sized(H, "H", n_tok, device=X.device, dtype=torch.float32)
+        workspace, wsb = _workspace(lib.estp_token_entropy_workspace_size(n_tok, d, V, dt), X.device, workspace)
+        _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(vocab_argmax),
+                                      _ptr(workspace), wsb, st), "estp_token_entropy")
     return H
+
+
+def _qk_shapes(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor):
+    if Q.dim() == 3:
+        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
+    _need(Q, "Q", ndim=4)
+    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
+    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
+    L, n_tok, Hq, dh = Q.shape
+    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
+        raise ValueError("Q and K shapes disagree")
+    return Q, K, L, n_tok, Hq, K.shape[2], dh
 
 
 def attn_importance(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, max_seqlen: int,
@@ -199,27 +227,19 @@ def attn_importance(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tensor, 
     Q [L, n_tok, Hq, dh], K [L, n_tok, Hkv, dh] (3-D tensors are one layer).
     """
     lib = load()
-    if Q.dim() == 3:
-        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
-    _need(Q, "Q", ndim=4)
-    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
-    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
-    L, n_tok, Hq, dh = Q.shape
-    Hkv = K.shape[2]
-    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
-        raise ValueError("Q and K shapes disagree")
+    Q, K, L, n_tok, Hq, Hkv, dh = _qk_shapes(Q, K, cu_seqlens)
     B = cu_seqlens.numel() - 1
     if scale is None:
         scale = 1.0 / math.sqrt(dh)
-    if S is None:
-        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
-    ws = lib.estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
-    workspace, wsb = _workspace(ws, Q.device, workspace)
-    with torch.cuda.device(Q.device):
+    with _on(stream, Q.device) as st:
+        if S is None:
+            S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+        _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
+        ws = lib.estp_attn_importance_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
+        workspace, wsb = _workspace(ws, Q.device, workspace)
         _check(lib.estp_attn_importance(_ptr(Q), _ptr(K), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L, Hq, Hkv, dh,
-                                        float(scale), dt, _ptr(S), _ptr(workspace), wsb, _stream(stream, Q.device)),
+                                        float(scale), dt, _ptr(S), _ptr(workspace), wsb, st),
                "estp_attn_importance")
     return S
 
@@ -232,33 +252,25 @@ def attn_importance_from_lse(Q: torch.Tensor, K: torch.Tensor, lse: torch.Tensor
     Q [L, n_tok, Hq, dh], K [L, n_tok, Hkv, dh] (3-D tensors and a 2-D ``lse`` are one layer).
     """
     lib = load()
-    if Q.dim() == 3:
-        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
+    Q, K, L, n_tok, Hq, Hkv, dh = _qk_shapes(Q, K, cu_seqlens)
     if lse.dim() == 2:
         lse = lse.unsqueeze(0)
-    _need(Q, "Q", ndim=4)
-    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
     _need(lse, "lse", device=Q.device, dtype=torch.float32, ndim=3)
-    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
-    L, n_tok, Hq, dh = Q.shape
-    Hkv = K.shape[2]
-    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
-        raise ValueError("Q and K shapes disagree")
     if tuple(lse.shape) != (L, Hq, n_tok):
         raise ValueError(f"lse must be [L, Hq, n_tok] = {(L, Hq, n_tok)}, got {tuple(lse.shape)}")
     B = cu_seqlens.numel() - 1
     if scale is None:
         scale = 1.0 / math.sqrt(dh)
-    if S is None:
-        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
-    ws = lib.estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
-    workspace, wsb = _workspace(ws, Q.device, workspace)
-    with torch.cuda.device(Q.device):
+    with _on(stream, Q.device) as st:
+        if S is None:
+            S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+        _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
+        ws = lib.estp_attn_importance_from_lse_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt)
+        workspace, wsb = _workspace(ws, Q.device, workspace)
         _check(lib.estp_attn_importance_from_lse(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen),
                                                  n_tok, L, Hq, Hkv, dh, float(scale), dt, _ptr(S), _ptr(workspace),
-                                                 wsb, _stream(stream, Q.device)),
+                                                 wsb, st),
                "estp_attn_importance_from_lse")
     return S
 
@@ -271,15 +283,7 @@ def attn_importance_ex(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tenso
     ``lse`` [L, Hq, n_tok], per-layer weights (host sequence of L floats), and the diagonal
     left out of the column sums (``exclude_self``)."""
     lib = load()
-    if Q.dim() == 3:
-        Q, K = Q.unsqueeze(0), K.unsqueeze(0)
-    _need(Q, "Q", ndim=4)
-    _need(K, "K", device=Q.device, dtype=Q.dtype, ndim=4)
-    _need(cu_seqlens, "cu_seqlens", device=Q.device, dtype=torch.int32, ndim=1)
-    L, n_tok, Hq, dh = Q.shape
-    Hkv = K.shape[2]
-    if K.shape[0] != L or K.shape[1] != n_tok or K.shape[3] != dh:
-        raise ValueError("Q and K shapes disagree")
+    Q, K, L, n_tok, Hq, Hkv, dh = _qk_shapes(Q, K, cu_seqlens)
     if lse is not None:
         if lse.dim() == 2:
             lse = lse.unsqueeze(0)
@@ -294,17 +298,18 @@ def attn_importance_ex(Q: torch.Tensor, K: torch.Tensor, cu_seqlens: torch.Tenso
     B = cu_seqlens.numel() - 1
     if scale is None:
         scale = 1.0 / math.sqrt(dh)
-    if S is None:
-        S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
-    _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
     dt = _dtype_code(Q)
-    ws = lib.estp_attn_importance_ex_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt, int(lse is not None))
-    workspace, wsb = _workspace(ws, Q.device, workspace)
     flags = ESTP_IMPORTANCE_EXCLUDE_SELF if exclude_self else 0
-    with torch.cuda.device(Q.device):
+    with _on(stream, Q.device) as st:
+        if S is None:
+            S = torch.empty(n_tok, dtype=torch.float32, device=Q.device)
+        _sized(S, "S", n_tok, device=Q.device, dtype=torch.float32)
+        ws = lib.estp_attn_importance_ex_workspace_size(n_tok, B, max_seqlen, L, Hq, Hkv, dh, dt,
+                                                        int(lse is not None))
+        workspace, wsb = _workspace(ws, Q.device, workspace)
         _check(lib.estp_attn_importance_ex(_ptr(Q), _ptr(K), _ptr(lse), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, L,
                                            Hq, Hkv, dh, float(scale), lw, flags, dt, _ptr(S), _ptr(workspace), wsb,
-                                           _stream(stream, Q.device)),
+                                           st),
                "estp_attn_importance_ex")
     return S
 
@@ -325,24 +330,24 @@ def combine_pool(X: torch.Tensor, S: torch.Tensor, H: torch.Tensor, cu_seqlens: 
     _sized(H, "H", n_tok, device=X.device, dtype=torch.float32)
     _need(cu_seqlens, "cu_seqlens", device=X.device, dtype=torch.int32, ndim=1)
     B = cu_seqlens.numel() - 1
-    if pooled is None:
-        pooled = torch.empty(B, d, dtype=torch.float32, device=X.device)
-    _sized(pooled, "pooled", B * d, device=X.device, dtype=torch.float32)
-    if e is None and want_e:
-        e = torch.empty(n_tok, dtype=torch.float32, device=X.device)
-    if e is not None:
-        _sized(e, "e", n_tok, device=X.device, dtype=torch.float32)
-    if top is None and want_top:
-        top = torch.empty(B, dtype=torch.int32, device=X.device)
-    if top is not None:
-        _sized(top, "top", B, device=X.device, dtype=torch.int32)
     dt = _dtype_code(X)
-    workspace, wsb = _workspace(lib.estp_combine_pool_workspace_size(n_tok, B, max_seqlen, d, dt), X.device,
-                                workspace)
-    with torch.cuda.device(X.device):
+    with _on(stream, X.device) as st:
+        if pooled is None:
+            pooled = torch.empty(B, d, dtype=torch.float32, device=X.device)
+        _sized(pooled, "pooled", B * d, device=X.device, dtype=torch.float32)
+        if e is None and want_e:
+            e = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+        if e is not None:
+            _sized(e, "e", n_tok, device=X.device, dtype=torch.float32)
+        if top is None and want_top:
+            top = torch.empty(B, dtype=torch.int32, device=X.device)
+        if top is not None:
+            _sized(top, "top", B, device=X.device, dtype=torch.int32)
+        workspace, wsb = _workspace(lib.estp_combine_pool_workspace_size(n_tok, B, max_seqlen, d, dt), X.device,
+                                    workspace)
         _check(lib.estp_combine_pool(_ptr(X), _ptr(S), _ptr(H), _ptr(cu_seqlens), B, int(max_seqlen), n_tok, d,
                                      float(lambda1), float(lambda2), float(alpha), NORMS[norm], dt, _ptr(pooled),
-                                     _ptr(e), _ptr(top), _ptr(workspace), wsb, _stream(stream, X.device)),
+                                     _ptr(e), _ptr(top), _ptr(workspace), wsb, st),
                "estp_combine_pool")
     return pooled, e, top
 
@@ -362,14 +367,14 @@ def predict(pooled: torch.Tensor, W1: torch.Tensor, b1: Optional[torch.Tensor], 
     for t, n, size in ((b1, "b1", Hd), (b2, "b2", K), (centres, "centres", K)):
         if t is not None:
             _sized(t, n, size, device=pooled.device, dtype=torch.float32)
-    yhat = torch.empty(B, dtype=torch.float32, device=pooled.device)
-    bins = torch.empty(B, dtype=torch.int32, device=pooled.device) if K > 1 else None
-    order = torch.empty(B, dtype=torch.int32, device=pooled.device) if want_order else None
-    workspace, wsb = _workspace(lib.estp_predict_workspace_size(B, d, Hd, K), pooled.device, workspace)
-    with torch.cuda.device(pooled.device):
+    with _on(stream, pooled.device) as st:
+        yhat = torch.empty(B, dtype=torch.float32, device=pooled.device)
+        bins = torch.empty(B, dtype=torch.int32, device=pooled.device) if K > 1 else None
+        order = torch.empty(B, dtype=torch.int32, device=pooled.device) if want_order else None
+        workspace, wsb = _workspace(lib.estp_predict_workspace_size(B, d, Hd, K), pooled.device, workspace)
         _check(lib.estp_predict(_ptr(pooled), B, d, _ptr(W1), _ptr(b1), Hd, ACTS[act], _ptr(W2), _ptr(b2), K,
-                                _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb,
-                                _stream(stream, pooled.device)), "estp_predict")
+                                _ptr(centres), _ptr(yhat), _ptr(bins), _ptr(order), _ptr(workspace), wsb, st),
+               "estp_predict")
     return yhat, bins, order
 
 
@@ -402,15 +407,15 @@ def head_train_step(pooled: torch.Tensor, y: torch.Tensor, edges: torch.Tensor, 
     n = hidden * d + hidden + K * hidden + K
     if theta.numel() != n or m.numel() != n or v.numel() != n:
         raise ValueError(f"theta, m, v must hold {n} values")
-    if loss is None:
-        loss = torch.empty(1, dtype=torch.float32, device=dev_)
-    _sized(loss, "loss", 1, device=dev_, dtype=torch.float32)
-    workspace, wsb = _workspace(lib.estp_head_train_step_workspace_size(B, d, hidden, K), dev_, workspace)
-    with torch.cuda.device(dev_):
+    with _on(stream, dev_) as st:
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float32, device=dev_)
+        _sized(loss, "loss", 1, device=dev_, dtype=torch.float32)
+        workspace, wsb = _workspace(lib.estp_head_train_step_workspace_size(B, d, hidden, K), dev_, workspace)
         _check(lib.estp_head_train_step(_ptr(pooled), _ptr(y), B, d, hidden, K, ACTS[act], _ptr(edges), _ptr(centres),
                                         _ptr(theta), _ptr(m), _ptr(v), int(step), float(lambda3), float(lr),
                                         float(beta1), float(beta2), float(eps), float(weight_decay), _ptr(loss),
-                                        _ptr(workspace), wsb, _stream(stream, dev_)),
+                                        _ptr(workspace), wsb, st),
                "estp_head_train_step")
     return loss
 
@@ -424,10 +429,10 @@ def misalignment(H: torch.Tensor, S: torch.Tensor, cu_seqlens: torch.Tensor, fra
     _sized(S, "S", H.numel(), device=H.device, dtype=torch.float32)
     _need(cu_seqlens, "cu_seqlens", device=H.device, dtype=torch.int32, ndim=1)
     B = cu_seqlens.numel() - 1
-    counts = torch.empty(B, 4, dtype=torch.int32, device=H.device)
-    with torch.cuda.device(H.device):
+    with _on(stream, H.device) as st:
+        counts = torch.empty(B, 4, dtype=torch.int32, device=H.device)
         _check(lib.estp_misalignment(_ptr(H), _ptr(S), _ptr(cu_seqlens), B, float(frac_low), float(frac_high),
-                                     _ptr(counts), _stream(stream, H.device)), "estp_misalignment")
+                                     _ptr(counts), st), "estp_misalignment")
     return counts
 
 
@@ -437,9 +442,8 @@ def sjf_padding(lengths: torch.Tensor, order: Optional[torch.Tensor], batch: int
     _need(lengths, "lengths", dtype=torch.int32, ndim=1)
     if order is not None:
         _sized(order, "order", lengths.numel(), device=lengths.device, dtype=torch.int32)
-    out = torch.empty(3, dtype=torch.int64, device=lengths.device)
-    with torch.cuda.device(lengths.device):
-        _check(lib.estp_sjf_padding(_ptr(lengths), _ptr(order), lengths.numel(), int(batch), _ptr(out),
-                                    _stream(stream, lengths.device)),
+    with _on(stream, lengths.device) as st:
+        out = torch.empty(3, dtype=torch.int64, device=lengths.device)
+        _check(lib.estp_sjf_padding(_ptr(lengths), _ptr(order), lengths.numel(), int(batch), _ptr(out), st),
                "estp_sjf_padding")
     return out

@@ -29,7 +29,11 @@
 // folding of a finished tile into the running per-token state (max, sum
 // 2^(z2-m), sum 2^(z2-m)(z2-m), base-2 units) overlaps the loads of the next
 // tile.  The n_vsplit partial states per token are merged by a second small
-// kernel that writes H.  Workgroup ids are remapped so the 32 workgroups
+// kernel that writes H.  When the caller asks for the most probable next
+// token as well, a template variant of the kernel also keeps, per token
+// column, the largest logit and its lowest vocabulary index; the same merges
+// carry it (the variant without it is the plain kernel).  Workgroup ids are
+// remapped so the 32 workgroups
 // resident on one XCD (ids are dealt round-robin over the 8 XCDs) cover 4
 // vocabulary slices x 8 token tiles, and one dispatch wave of 256 covers
 // 16 x 16: concurrent workgroups stream the same W and X tiles through that
@@ -81,6 +85,14 @@ __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Largest logit with its vocabulary index: b wins over a when it is larger, or
+// equal with a lower index (ties go to the lowest index).
+__device__ __forceinline__ void arg_merge(float& av, int& ai, float bv, int bi) {
+  const bool take = bv > av || (bv == av && bi < ai);
+  av = take ? bv : av;
+  ai = take ? bi : ai;
+}
+
 // A stage is BK deep (kSub k steps).  Ring of P part slots: part 2s + 0 / 2s + 1
 // (W / X of stage s) lives in slot (2s + o) % P.  Within a stage the wave runs
 // kSub k steps, each reading the next step's fragments while its MFMAs run.
@@ -89,10 +101,11 @@ __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, 
 // after it the two freed slots take parts 2s + P and 2s + P + 1.  With P odd
 // the W part of a stage is issued one stage before its X part, and about
 // (P - 2) / 2 stages of loads are in flight while a stage is consumed.
-template <int P, int BK>
+template <int P, int BK, bool kArg>
 __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int n_tok, int d, int V, int n_vsplit,
-    int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t) {
+    int n_vt, int n_tt, float* __restrict__ part_m, float* __restrict__ part_s, float* __restrict__ part_t,
+    float* __restrict__ part_zmax, int* __restrict__ part_arg) {
   using G = Geom<BK>;
   constexpr int L = G::L;
   constexpr int kSub = G::kSub;
@@ -226,6 +239,12 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
   Ent2 st[kNB];
 #pragma unroll
   for (int j = 0; j < kNB; ++j) st[j] = Ent2{-INFINITY, 0.f, 0.f};
+  // mode tracking (kArg): the largest logit seen per token column and its vocabulary index.
+  // The four lanes fq = 0..3 that share a column merge their candidates after every tile,
+  // and lane fq keeps columns 2 fq and 2 fq + 1 only: 4 registers instead of 16, which the
+  // fold's register budget needs.
+  float zmax[2] = {-INFINITY, -INFINITY};
+  int zarg[2] = {INT32_MAX, INT32_MAX};
 
   // ---- prologue: the first parts in flight; wait for stage 0, read its first fragments
 #pragma unroll
@@ -375,6 +394,31 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
           }
         e = Ent2{mnew, s, t};
       }
+      if (kArg) {
+        // the tile's largest live logit in this column and its row.  The lane's rows are visited
+        // in ascending order, so a strict compare keeps the lowest index among equal logits.
+        // (One separate pass after the fold: a compare inside the fold's two paths overflows the
+        // registers.)
+        float tb = -INFINITY;
+        int ti = 0;
+#pragma unroll
+        for (int i = 0; i < kNB; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool up = (!ragged || i * 16 + r < lim) && acc[i][j][r] > tb;
+            tb = up ? acc[i][j][r] : tb;
+            ti = up ? i * 16 + r : ti;
+          }
+        // the column's candidate over the four lanes that share it, then kept by lane j / 2
+        float cb = tb;
+        int ci = vt * kBV + wv * 128 + 4 * fq + ti;
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) arg_merge(cb, ci, __shfl_xor(cb, o, 64), __shfl_xor(ci, o, 64));
+        if (fq == j / 2 && cb > zmax[j & 1]) {  // strict: an earlier tile keeps equal maxima
+          zmax[j & 1] = cb;
+          zarg[j & 1] = ci;
+        }
+      }
       // rebase to the running log-sum-exp: m += log2 s, s = 1, t = t / s - log2 s
       // (s >= 1 here: the reference never exceeds the largest logit seen, in base 2)
       if (e.s > 0.f) {
@@ -402,14 +446,23 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
   // zeros into their slots) must land before slot 0 is reused.
   wait_vm<0>();
   __syncthreads();  // every wave is done with the ring and no transfer remains in flight
-  float* xbuf = reinterpret_cast<float*>(lds);  // [BT tokens][3]
+  constexpr int kSt = kArg ? 5 : 3;                // floats per token in the exchange
+  float* xbuf = reinterpret_cast<float*>(lds);  // [BT tokens][kSt]
   if (wv == 1 && fq == 0) {
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
-      float* p = xbuf + (wt * 128 + j * 16 + fr) * 3;
+      float* p = xbuf + (wt * 128 + j * 16 + fr) * kSt;
       p[0] = st[j].m;
       p[1] = st[j].s;
       p[2] = st[j].t;
+    }
+  }
+  if (kArg && wv == 1) {  // lane fq holds columns 2 fq and 2 fq + 1
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float* p = xbuf + (wt * 128 + (2 * fq + c) * 16 + fr) * kSt;
+      p[3] = zmax[c];
+      p[4] = __int_as_float(zarg[c]);
     }
   }
   __syncthreads();
@@ -417,7 +470,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       const int tl = wt * 128 + j * 16 + fr;
-      const float* p = xbuf + tl * 3;
+      const float* p = xbuf + tl * kSt;
       Ent2 r = ent2_merge(st[j], Ent2{p[0], p[1], p[2]});
       const int tok = tt * kBT + tl;
       if (tok < n_tok) {
@@ -428,14 +481,34 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
       }
     }
   }
+  if (kArg && wv == 0) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int tl = wt * 128 + (2 * fq + c) * 16 + fr;
+      const int tok = tt * kBT + tl;
+      if (tok < n_tok) {
+        const float* p = xbuf + tl * kSt;
+        float zb = zmax[c];
+        int ib = zarg[c];
+        arg_merge(zb, ib, p[3], __float_as_int(p[4]));
+        const size_t o = size_t(vs) * n_tok + tok;
+        part_zmax[o] = zb;
+        part_arg[o] = ib;
+      }
+    }
+  }
 }
 
 // Merge the n_vsplit partial states of each token and write H in nats:
-// H = ln2 * (log2 s - t / s).
+// H = ln2 * (log2 s - t / s).  With `arg` non-null, also the vocabulary index
+// of the largest logit over the slices (lowest index among equal maxima).
 __global__ __launch_bounds__(256) void entropy_merge_kernel(const float* __restrict__ part_m,
                                                             const float* __restrict__ part_s,
-                                                            const float* __restrict__ part_t, int n_tok,
-                                                            int n_vsplit, float* __restrict__ H) {
+                                                            const float* __restrict__ part_t,
+                                                            const float* __restrict__ part_zmax,
+                                                            const int* __restrict__ part_arg, int n_tok,
+                                                            int n_vsplit, float* __restrict__ H,
+                                                            int32_t* __restrict__ arg) {
   const int tok = blockIdx.x * 256 + threadIdx.x;
   if (tok >= n_tok) return;
   Ent2 a{part_m[tok], part_s[tok], part_t[tok]};
@@ -444,6 +517,15 @@ __global__ __launch_bounds__(256) void entropy_merge_kernel(const float* __restr
     a = ent2_merge(a, Ent2{part_m[o], part_s[o], part_t[o]});
   }
   H[tok] = kLn2 * (fast_log2(a.s) - a.t / a.s);
+  if (arg) {
+    float zb = part_zmax[tok];
+    int ib = part_arg[tok];
+    for (int v = 1; v < n_vsplit; ++v) {
+      const size_t o = size_t(v) * n_tok + tok;
+      arg_merge(zb, ib, part_zmax[o], part_arg[o]);
+    }
+    arg[tok] = ib;
+  }
 }
 
 int choose_vsplit(int n_vt) { return n_vt < kMaxVsplit ? n_vt : kMaxVsplit; }
@@ -460,12 +542,14 @@ extern "C" size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, in
   if (n_tok < 1 || V < 1) return 0;
   const int n_vt = (V + kBV - 1) / kBV;
   Carver c(nullptr);
-  for (int i = 0; i < 3; ++i) c.take<float>(size_t(choose_vsplit(n_vt)) * n_tok);
+  // per-slice (m, s, t) states, then the per-slice largest logit and its index
+  for (int i = 0; i < 5; ++i) c.take<float>(size_t(choose_vsplit(n_vt)) * n_tok);
   return c.bytes();
 }
 
 extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
-                                  float* H, void* workspace, size_t workspace_bytes, void* stream) {
+                                  float* H, int32_t* vocab_argmax, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
   clear_error();
   ESTP_REQUIRE(X && W && H, ESTP_ERR_INVALID_ARG, "estp_token_entropy: X, W and H must be non-null");
   ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG,
@@ -481,6 +565,8 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
                "estp_token_entropy: d = %d too large", d);
   ESTP_REQUIRE(aligned(X, 16) && aligned(W, 16), ESTP_ERR_INVALID_ARG,
                "estp_token_entropy: X and W must be 16-byte aligned");
+  ESTP_REQUIRE(aligned(H, 4) && aligned(vocab_argmax, 4), ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: H and vocab_argmax must be 4-byte aligned");
   const size_t need = estp_token_entropy_workspace_size(n_tok, d, V, dtype);
   ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
                "estp_token_entropy: workspace of %zu bytes, %zu needed", workspace_bytes, need);
@@ -498,25 +584,38 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pm = c.take<float>(size_t(n_vsplit) * n);
   float* ps = c.take<float>(size_t(n_vsplit) * n);
   float* pt = c.take<float>(size_t(n_vsplit) * n);
+  float* pz = c.take<float>(size_t(n_vsplit) * n);
+  int* pa = c.take<int>(size_t(n_vsplit) * n);
+  const bool want_arg = vocab_argmax != nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   if (dtype == ESTP_F32) {
     launch_entropy_f32(static_cast<const float*>(X), static_cast<const float*>(W), n, int(d), int(V), n_vsplit, pm,
-                       ps, pt, s);
+                       ps, pt, pz, want_arg ? pa : nullptr, s);
     ESTP_CHECK_LAUNCH("entropy_f32_kernel");
-    entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
-    ESTP_CHECK_LAUNCH("entropy_merge_kernel");
-    return ESTP_OK;
+  } else {
+    const dim3 grid(n_vsplit * n_tt), block(kWaves * 64);
+    const uint16_t* Xh = static_cast<const uint16_t*>(X);
+    const uint16_t* Wh = static_cast<const uint16_t*>(W);
+    if (d % 64 == 0) {
+      if (want_arg)
+        entropy_gemm_kernel<5, 64, true><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
+                                                                ps, pt, pz, pa);
+      else
+        entropy_gemm_kernel<5, 64, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
+                                                                 ps, pt, nullptr, nullptr);
+    } else {
+      if (want_arg)
+        entropy_gemm_kernel<9, 32, true><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
+                                                                ps, pt, pz, pa);
+      else
+        entropy_gemm_kernel<9, 32, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
+                                                                 ps, pt, nullptr, nullptr);
+    }
+    ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   }
-  const dim3 grid(n_vsplit * n_tt), block(kWaves * 64);
-  const uint16_t* Xh = static_cast<const uint16_t*>(X);
-  const uint16_t* Wh = static_cast<const uint16_t*>(W);
-  if (d % 64 == 0)
-    entropy_gemm_kernel<5, 64><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
-  else
-    entropy_gemm_kernel<9, 32><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm, ps, pt);
-  ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
-  entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, n, n_vsplit, H);
+  entropy_merge_kernel<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(pm, ps, pt, pz, want_arg ? pa : nullptr, n,
+                                                                   n_vsplit, H, vocab_argmax);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");
   return ESTP_OK;
 }

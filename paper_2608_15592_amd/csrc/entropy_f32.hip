@@ -14,7 +14,8 @@
 // own max).  At the end the 16 threads that share a token column merge their
 // states (two lane exchanges, then the four waves through LDS, in a fixed
 // order) and the slice writes the partial layout that entropy_merge_kernel
-// reduces.
+// reduces.  The kArg variant also keeps each token column's largest logit and
+// its lowest vocabulary index through the same merges.
 #include "estp_common.h"
 #include "f32_paths.h"
 
@@ -33,12 +34,22 @@ static_assert(kFPitch % 4 == 0 && kFPitch >= kFV, "pitch");
 
 }  // namespace
 
+// b replaces a when larger, or equal with a lower index.
+__device__ __forceinline__ void arg_merge_f32(float& av, int& ai, float bv, int bi) {
+  const bool take = bv > av || (bv == av && bi < ai);
+  av = take ? bv : av;
+  ai = take ? bi : ai;
+}
+
+template <bool kArg>
 __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __restrict__ X,
                                                                 const float* __restrict__ W, int n_tok, int d,
                                                                 int V, int n_vsplit, int n_vt,
                                                                 float* __restrict__ part_m,
                                                                 float* __restrict__ part_s,
-                                                                float* __restrict__ part_t) {
+                                                                float* __restrict__ part_t,
+                                                                float* __restrict__ part_zmax,
+                                                                int* __restrict__ part_arg) {
   __shared__ __attribute__((aligned(16))) float ws[2][kFK][kFPitch];
   __shared__ __attribute__((aligned(16))) float xs[2][kFK][kFPitch];
   const int tid = threadIdx.x;
@@ -88,6 +99,13 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
   Ent2 st[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) st[j] = Ent2{-INFINITY, 0.f, 0.f};
+  float zmax[8];  // kArg: largest logit per token column and its vocabulary index
+  int zarg[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    zmax[j] = -INFINITY;
+    zarg[j] = INT32_MAX;
+  }
 
   load(0);
   store(0);
@@ -118,9 +136,18 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         float mx = -INFINITY;
+        int imx = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (valid[i]) mx = fmaxf(mx, acc[i][j]);
+        for (int i = 0; i < 8; ++i) {
+          // rows ascend with i: a strict compare keeps the lowest index among equal logits
+          const bool up = valid[i] && acc[i][j] > mx;
+          imx = up ? i : imx;
+          mx = up ? acc[i][j] : mx;
+        }
+        if (kArg && mx > zmax[j]) {
+          zmax[j] = mx;
+          zarg[j] = v0 + (imx < 4 ? 4 * rv + imx : 64 + 4 * rv + imx - 4);
+        }
         if (valid[0]) {  // row 4 rv of the tile is the thread's first; none valid -> nothing to add
           const float m2 = mx * kLog2e;
           float s = 0.f, t = 0.f;
@@ -149,10 +176,12 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
     for (int o = 16; o <= 32; o <<= 1) {
       const Ent2 other{__shfl_xor(st[j].m, o, 64), __shfl_xor(st[j].s, o, 64), __shfl_xor(st[j].t, o, 64)};
       st[j] = ent2_merge(st[j], other);
+      if (kArg) arg_merge_f32(zmax[j], zarg[j], __shfl_xor(zmax[j], o, 64), __shfl_xor(zarg[j], o, 64));
     }
   }
   // ... and so do the four waves: merged through LDS (the stage buffers are free after the last barrier)
-  float* red = &ws[0][0][0];  // [3][4 waves][128 tokens]
+  float* red = &ws[0][0][0];  // [3 (5 with kArg)][4 waves][128 tokens]
+  static_assert(5 * 4 * kFT <= 2 * kFK * kFPitch, "exchange fits in the stage buffer");
   const int wave = tid >> 6, lane = tid & 63;
   if (lane < 16) {
 #pragma unroll
@@ -161,6 +190,10 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
       red[(0 * 4 + wave) * kFT + col] = st[j].m;
       red[(1 * 4 + wave) * kFT + col] = st[j].s;
       red[(2 * 4 + wave) * kFT + col] = st[j].t;
+      if (kArg) {
+        red[(3 * 4 + wave) * kFT + col] = zmax[j];
+        red[(4 * 4 + wave) * kFT + col] = __int_as_float(zarg[j]);
+      }
     }
   }
   __syncthreads();
@@ -172,6 +205,13 @@ __global__ __launch_bounds__(kFThreads) void entropy_f32_kernel(const float* __r
     part_m[o] = a.m;
     part_s[o] = a.s;
     part_t[o] = a.t;
+    if (kArg) {
+      float zb = red[12 * kFT + tid];
+      int ib = __float_as_int(red[16 * kFT + tid]);
+      for (int w = 1; w < 4; ++w) arg_merge_f32(zb, ib, red[(12 + w) * kFT + tid], __float_as_int(red[(16 + w) * kFT + tid]));
+      part_zmax[o] = zb;
+      part_arg[o] = ib;
+    }
   }
 }
 
@@ -180,11 +220,16 @@ size_t entropy_f32_workgroups(int n_tok, int n_vsplit) {
 }
 
 void launch_entropy_f32(const float* X, const float* W, int n_tok, int d, int V, int n_vsplit, float* part_m,
-                        float* part_s, float* part_t, hipStream_t s) {
+                        float* part_s, float* part_t, float* part_zmax, int* part_arg, hipStream_t s) {
   const int n_vt = (V + kFV - 1) / kFV;
   const int n_tt = (n_tok + kFT - 1) / kFT;
-  entropy_f32_kernel<<<dim3(n_vsplit * n_tt), dim3(kFThreads), 0, s>>>(X, W, n_tok, d, V, n_vsplit, n_vt, part_m,
-                                                                       part_s, part_t);
+  const dim3 grid(n_vsplit * n_tt), block(kFThreads);
+  if (part_arg)
+    entropy_f32_kernel<true><<<grid, block, 0, s>>>(X, W, n_tok, d, V, n_vsplit, n_vt, part_m, part_s, part_t,
+                                                    part_zmax, part_arg);
+  else
+    entropy_f32_kernel<false><<<grid, block, 0, s>>>(X, W, n_tok, d, V, n_vsplit, n_vt, part_m, part_s, part_t,
+                                                     nullptr, nullptr);
 }
 
 }  // namespace detail

@@ -14,9 +14,11 @@ namespace detail {
 // Workgroups in launch_entropy_f32's grid.
 size_t entropy_f32_workgroups(int n_tok, int n_vsplit);
 // Per-slice online-softmax partial states (part_m/s/t [n_vsplit, n_tok], base
-// 2) of the logits W x for every token; 1 <= n_vsplit <= ceil(V / 128).
+// 2) of the logits W x for every token; 1 <= n_vsplit <= ceil(V / 128).  With
+// part_arg non-null, also each slice's largest logit (part_zmax) and its
+// lowest vocabulary index (part_arg), same layout.
 void launch_entropy_f32(const float* X, const float* W, int n_tok, int d, int V, int n_vsplit, float* part_m,
-                        float* part_s, float* part_t, hipStream_t s);
+                        float* part_s, float* part_t, float* part_zmax, int* part_arg, hipStream_t s);
 
 // The two importance passes over the same grid as the bf16 kernels: n_rows
 // 256-row block entries (from `blist`, n_bound entries, when non-null; else the

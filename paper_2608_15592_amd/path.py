@@ -17,16 +17,20 @@ def run_path(X: torch.Tensor, W: torch.Tensor, Q: torch.Tensor, K: torch.Tensor,
     ``head`` is ``(W1, b1, W2, b2, centres)``.  ``bufs`` (optional) holds
     preallocated outputs and workspaces keyed by name so that repeated calls
     allocate nothing: H, S, pooled, e, top, ws_entropy, ws_importance, ws_pool,
-    ws_predict.
+    ws_predict; an int32 [n_tok] ``vocab_argmax`` entry, when present, also
+    receives each token's most probable next token.
     """
     b = bufs if bufs is not None else {}
-    H = _lib.token_entropy(X, W, H=b.get("H"), workspace=b.get("ws_entropy"), stream=stream)
+    H = _lib.token_entropy(X, W, H=b.get("H"), workspace=b.get("ws_entropy"), stream=stream,
+                           vocab_argmax=b.get("vocab_argmax"))
     S = _lib.attn_importance(Q, K, cu_seqlens, max_seqlen, scale=scale, S=b.get("S"),
                              workspace=b.get("ws_importance"), stream=stream)
     pooled, e, top = _lib.combine_pool(X, S, H, cu_seqlens, max_seqlen, lambda1, lambda2, alpha, norm,
                                        pooled=b.get("pooled"), e=b.get("e"), top=b.get("top"),
                                        workspace=b.get("ws_pool"), stream=stream)
     out = {"H": H, "S": S, "pooled": pooled, "e": e, "top": top}
+    if b.get("vocab_argmax") is not None:
+        out["vocab_argmax"] = b["vocab_argmax"]
     if head is not None:
         W1, b1, W2, b2, centres = head
         out["yhat"], out["bin"], out["order"] = _lib.predict(pooled, W1, b1, W2, b2, centres, act,

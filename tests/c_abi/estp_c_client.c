@@ -32,7 +32,7 @@ static int host_checks(void) {
   if (strlen(estp_status_string(ESTP_ERR_INVALID_ARG)) == 0) return fail("estp_status_string");
   ws = estp_token_entropy_workspace_size(100, 64, 1000, ESTP_BF16);
   if (ws == 0) return fail("estp_token_entropy_workspace_size");
-  if (estp_token_entropy(NULL, NULL, 100, 64, 1000, ESTP_BF16, NULL, NULL, ws, NULL) != ESTP_ERR_INVALID_ARG)
+  if (estp_token_entropy(NULL, NULL, 100, 64, 1000, ESTP_BF16, NULL, NULL, NULL, ws, NULL) != ESTP_ERR_INVALID_ARG)
     return fail("null inputs not rejected");
   if (estp_last_error()[0] == '\0') return fail("no error message");
   if (estp_attn_importance(NULL, NULL, NULL, 1, 1, 1, 1, 1, 1, 64, 0.125f, ESTP_BF16, NULL, NULL, 0, NULL) !=
@@ -89,7 +89,7 @@ static int entropy_uniform(int dtype) {
   HIP_OK(hipMalloc((void**)&H, (size_t)n * sizeof(float)));
   wsb = estp_token_entropy_workspace_size(n, d, V, dtype);
   HIP_OK(hipMalloc(&ws, wsb));
-  if (estp_token_entropy(X, W, n, d, V, dtype, H, ws, wsb, NULL) != ESTP_OK) return fail("estp_token_entropy");
+  if (estp_token_entropy(X, W, n, d, V, dtype, H, NULL, ws, wsb, NULL) != ESTP_OK) return fail("estp_token_entropy");
   HIP_OK(hipDeviceSynchronize());
   HIP_OK(hipMemcpy(h, H, (size_t)n * sizeof(float), hipMemcpyDeviceToHost));
   for (i = 0; i < (size_t)n; ++i) err = fmax(err, fabs((double)h[i] - log((double)V)));

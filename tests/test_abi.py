@@ -53,16 +53,17 @@ def test_entropy_validation():
     ws = lib.estp_token_entropy_workspace_size(100, 64, 1000, 0)
     assert ws > 0
     cases = [
-        ((None, FAKE, 100, 64, 1000, 0, FAKE, WS, ws, None), 1),        # null X
-        ((FAKE, FAKE, 0, 64, 1000, 0, FAKE, WS, ws, None), 1),          # n_tok < 1
-        ((FAKE, FAKE, 100, 60, 1000, 0, FAKE, WS, ws, None), 1),        # d % 8
-        ((FAKE, FAKE, 100, 64, 0, 0, FAKE, WS, ws, None), 1),           # V < 1
-        ((FAKE, FAKE, 100, 64, 1000, 7, FAKE, WS, ws, None), 1),        # unknown dtype
-        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, WS, ws, None), 2),        # bf16: d not a multiple of 32
-        ((FAKE, FAKE, 100, 40, 1000, 1, FAKE, WS, ws - 1, None), 3),    # f32 takes any d % 8 == 0
-        ((UNALIGNED, FAKE, 100, 64, 1000, 0, FAKE, WS, ws, None), 1),   # alignment
-        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, WS, ws - 1, None), 3),    # workspace short
-        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, None, ws, None), 1),      # workspace null
+        ((None, FAKE, 100, 64, 1000, 0, FAKE, None, WS, ws, None), 1),        # null X
+        ((FAKE, FAKE, 0, 64, 1000, 0, FAKE, None, WS, ws, None), 1),          # n_tok < 1
+        ((FAKE, FAKE, 100, 60, 1000, 0, FAKE, None, WS, ws, None), 1),        # d % 8
+        ((FAKE, FAKE, 100, 64, 0, 0, FAKE, None, WS, ws, None), 1),           # V < 1
+        ((FAKE, FAKE, 100, 64, 1000, 7, FAKE, None, WS, ws, None), 1),        # unknown dtype
+        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, None, WS, ws, None), 2),        # bf16: d not a multiple of 32
+        ((FAKE, FAKE, 100, 40, 1000, 1, FAKE, None, WS, ws - 1, None), 3),    # f32 takes any d % 8 == 0
+        ((UNALIGNED, FAKE, 100, 64, 1000, 0, FAKE, None, WS, ws, None), 1),   # alignment
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, UNALIGNED, WS, ws, None), 1),   # argmax output alignment
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, None, WS, ws - 1, None), 3),    # workspace short
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, None, None, ws, None), 1),      # workspace null
     ]
     for args, code in cases:
         assert lib.estp_token_entropy(*args) == code, (args, lib.estp_last_error())
@@ -255,7 +256,7 @@ def test_launch_size_limits():
     lib = estp.load()
     n = 300_000_000  # bf16 entropy: 16 slices x ceil(n / 256) workgroups of 256 threads
     ws = lib.estp_token_entropy_workspace_size(n, 32, 4096, 0)
-    assert lib.estp_token_entropy(FAKE, FAKE, n, 32, 4096, 0, FAKE, WS, ws, None) == 2
+    assert lib.estp_token_entropy(FAKE, FAKE, n, 32, 4096, 0, FAKE, None, WS, ws, None) == 2
     assert b"launch" in lib.estp_last_error()
     n = 2_000_000_000  # importance: 2 x (n / 256) x L x Hq fp32 pass-1 workgroups
     ws = lib.estp_attn_importance_workspace_size(n, 1, n, 1, 2, 2, 64, 0)

@@ -63,3 +63,31 @@ def test_analyses_reject_mis_sized_inputs():
     lengths = torch.ones(10, dtype=torch.int32, device="cuda")
     with pytest.raises(ValueError, match="order must hold 10"):
         estp.sjf_padding(lengths, torch.arange(9, dtype=torch.int32, device="cuda"), 4)
+
+
+def test_side_stream_internal_workspace_is_not_reused_early():
+    # A call on a side stream with no workspace: the binding allocates workspace and outputs on
+    # that stream, so memory allocated and overwritten on the default stream right after the
+    # call returns can never land in blocks the side stream's kernels still use.
+    g = torch.Generator(device="cuda").manual_seed(3)
+    n, L, Hq, Hkv, dh = 4096, 2, 16, 4, 128
+    Q = torch.randn(L, n, Hq, dh, device="cuda", generator=g).to(torch.bfloat16)
+    K = torch.randn(L, n, Hkv, dh, device="cuda", generator=g).to(torch.bfloat16)
+    cu = _cu([2048, 1024, 1024])
+    X = torch.randn(n, 1024, device="cuda", generator=g).to(torch.bfloat16)
+    W = (0.02 * torch.randn(8192, 1024, device="cuda", generator=g)).to(torch.bfloat16)
+    ref_S = estp.attn_importance(Q, K, cu, 2048).clone()
+    ref_H = estp.token_entropy(X, W).clone()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    for _ in range(3):
+        side.wait_stream(torch.cuda.current_stream())
+        S = estp.attn_importance(Q, K, cu, 2048, stream=side)
+        H = estp.token_entropy(X, W, stream=side)
+        # immediately claim and scribble over memory on the default stream
+        junk = [torch.full((1 << 22,), float("nan"), device="cuda") for _ in range(8)]
+        side.synchronize()
+        torch.cuda.synchronize()
+        assert torch.equal(S, ref_S)
+        assert torch.equal(H, ref_H)
+        del junk, S, H

@@ -20,7 +20,7 @@ import oracle
 import paper_2608_15592_amd as estp
 import synth
 from synth import inputs as I
-from tests._util import dev, host, rel_l2
+from tests._util import check_vocab_argmax, dev, host, rel_l2
 
 pytestmark = pytest.mark.gpu
 
@@ -56,13 +56,22 @@ ENTROPY_F32_CASES = [
 def test_entropy_f32_parity(n, d, V, std, tag):
     X = _hidden(n, d, 1)
     W = _weight(V, d, 2, std)
-    H = host(estp.token_entropy(dev(X), dev(W)))
+    Xd, Wd = dev(X), dev(W)
+    H = host(estp.token_entropy(Xd, Wd))
     ref = oracle.token_entropy(X, W)
     err = np.abs(H.astype(np.float64) - ref)
     print(f"{tag}: max |dH| = {err.max():.3e} nats")
     assert err.max() <= H_TOL_F32
     if std == 0.0:
         np.testing.assert_allclose(H, np.log(V), rtol=0, atol=H_TOL_F32)
+    # the most probable next token from the same call: H unchanged, the mode exact (margin rule)
+    am = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    np.testing.assert_array_equal(host(estp.token_entropy(Xd, Wd, vocab_argmax=am)), H)
+    am = host(am)
+    counts = check_vocab_argmax(am, X, W)
+    print(f"{tag}: vocab argmax exact on {counts['exact']} rows, near ties {counts['tie']}")
+    if std == 0.0:
+        assert np.all(am == 0)
 
 
 def test_entropy_f32_repeatable_bitwise():

@@ -2,14 +2,19 @@
 bench.py times (the four calls back to back, preallocated workspaces).
 
 The oracle cannot redo a whole full-size batch in seconds, so each case checks:
-* exactly against the oracle: sampled entropy rows (including outlier tokens and both
-  ends), whole prompts for importance / pooled vector / length prediction / top token
-  where the oracle can afford them, and the last 256 keys of 32768-token prompts (their
-  importance needs only the last 256 attention rows);
-* on every prompt, properties that hold at any size: importance mass sums to L, weights
-  form a simplex and follow the fused scores, the pooled vector is the weighted sum of
-  the hidden states, and the shortest-job-first order sorts the predictions.
+* exactly against the oracle: sampled entropy rows and their most probable next token
+  (including outlier tokens and both ends), whole prompts for importance / pooled
+  vector / length prediction / top token where the oracle can afford them, the last
+  256 keys of 32768-token prompts (their importance needs only the last 256 attention
+  rows), and the first 256 keys and a middle block of a 32768-token prompt (every
+  row of the prompt reaches them: the longest column walks of the importance pass);
+* on every prompt: importance mass sums to L, and the oracle's fusion and pooling
+  (Eq. 3-5) applied to this call's own S and H give its weights, top token and pooled
+  vector; the shortest-job-first order sorts the predictions.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -19,7 +24,7 @@ import paper_2608_15592_amd as estp
 import synth
 from paper_2608_15592_amd.path import alloc_buffers
 from synth import inputs as I
-from tests._util import check_argmax_margin, dev, host, rel_l2
+from tests._util import check_argmax_margin, check_vocab_argmax, dev, host, rel_l2
 
 pytestmark = pytest.mark.gpu
 
@@ -36,6 +41,7 @@ def _run(w, seed=42):
     cu = dev(inp["cu_seqlens"])
     head = tuple(dev(inp[k]) for k in ("W1", "b1", "W2", "b2")) + (dev(inp["centres"]) if K > 1 else None,)
     bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, K, X.device)
+    bufs["vocab_argmax"] = torch.full((n_tok,), -1, dtype=torch.int32, device=X.device)
     out = estp.run_path(X, W, Q, Kk, cu, max_len, LAM1, LAM2, ALPHA, "none", head=head, bufs=bufs)
     torch.cuda.synchronize()
     got = {k: host(v) for k, v in out.items() if isinstance(v, torch.Tensor)}
@@ -60,23 +66,26 @@ def _entropy_rows(inp, got, n_rand=48, seed=0):
     err = np.abs(got["H"][rows] - ref).max()
     print(f"entropy: {len(rows)} sampled rows, max |dH| = {err:.2e}")
     assert err <= 2e-3
+    counts = check_vocab_argmax(got["vocab_argmax"][rows], inp["X"], inp["W"], rows)
+    print(f"vocab argmax: exact on {counts['exact']} sampled rows, near ties {counts['tie']}")
 
 
 def _properties(inp, got, w):
     cu = inp["cu_seqlens"].astype(np.int64)
     S, H, e = got["S"], got["H"], got["e"]
     assert np.all(np.isfinite(S)) and np.all(S > 0) and np.all(np.isfinite(H))
+    # component-wise: the oracle's Eq. 3-4 fed this call's own S and H must give its weights and
+    # top tokens, and the oracle's Eq. 5 fed those weights its pooled vectors (fp32 inputs to
+    # the fusion, so the bound is the fp32 one: exp of u with |du| ~ 1e-7 |u|)
+    ref_e, ref_top = oracle.combine_weights(S, H, cu, LAM1, LAM2, ALPHA, "none")
+    np.testing.assert_allclose(e, ref_e, rtol=1e-4, atol=1e-12)
     for b in range(len(cu) - 1):
         lo, hi = cu[b], cu[b + 1]
-        X = oracle.widen(inp["X"][lo:hi])
         assert abs(S[lo:hi].sum() - w.L) <= 1e-4 * w.L
         assert abs(e[lo:hi].sum() - 1.0) <= 1e-5
-        # weights follow the fused scores of this very call: e = softmax((l1 S + l2 H) / alpha)
-        u = (LAM1 * S[lo:hi].astype(np.float64) + LAM2 * H[lo:hi]) / ALPHA
-        ref_e = np.exp(u - u.max())
-        ref_e /= ref_e.sum()
-        np.testing.assert_allclose(e[lo:hi], ref_e, rtol=1e-4, atol=1e-12)
-        assert rel_l2(got["pooled"][b], e[lo:hi].astype(np.float64) @ X) <= 1e-5
+        check_argmax_margin(int(got["top"][b]) - lo, ref_e[lo:hi], 1e-4 * ref_e[lo:hi].max())
+        ref_p = oracle.pool(inp["X"][lo:hi], ref_e[lo:hi], [0, hi - lo])[0]
+        assert rel_l2(got["pooled"][b], ref_p) <= 1e-4
     y, order = got["yhat"], got["order"]
     assert sorted(order.tolist()) == list(range(len(y)))
     ys = y[order]
@@ -141,12 +150,34 @@ def test_fullsize_ragged_rl_batch():
     order = np.argsort(lengths, kind="stable")
     for b in (int(order[0]), int(order[1]), int(order[len(order) // 2])):  # two shortest and the median
         _exact_prompt(inp, got, w, b)
-    # the longest prompt's last 256 keys
+    # the longest prompt: its last 256 keys, and its first 256 keys (reached by every row)
     b = int(order[-1])
     cu = inp["cu_seqlens"].astype(np.int64)
     lo, hi = int(cu[b]), int(cu[b + 1])
     tail = oracle.attn_importance_tail(inp["Q"][:, lo:hi], inp["K"][:, lo:hi], hi - lo, 256)
     assert np.all(np.abs(got["S"][hi - 256:hi] - tail) <= 1e-3 * tail + 1e-12)
+    head = _keys_by_head(inp["Q"][:, lo:hi], inp["K"][:, lo:hi], hi - lo, np.arange(256), w.Hq)
+    print(f"longest prompt ({hi - lo} tokens): first 256 keys max rel dS = "
+          f"{(np.abs(got['S'][lo:lo + 256] - head) / head).max():.1e}")
+    assert np.all(np.abs(got["S"][lo:lo + 256] - head) <= 1e-3 * head + 1e-12)
+
+
+def _host_threads() -> int:
+    # the host share of one GPU on the test machines is 16 CPUs
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _keys_by_head(Qp, Kp, N, keys, Hq):
+    """oracle.attn_importance_keys for one prompt, its query heads spread over host threads
+    (each with single-threaded BLAS); the per-head parts add up to S at those keys."""
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1), ThreadPoolExecutor(_host_threads()) as ex:
+        parts = list(ex.map(lambda h: oracle.attn_importance_keys(Qp, Kp, N, keys, heads=[h]), range(Hq)))
+    return np.sum(parts, axis=0)
 
 
 def test_fullsize_long_context():
@@ -161,6 +192,31 @@ def test_fullsize_long_context():
         err = np.abs(got["S"][hi - 256:hi] - tail) / tail
         print(f"long prompt {b}: last 256 keys, max rel dS = {err.max():.1e}")
         assert np.all(np.abs(got["S"][hi - 256:hi] - tail) <= 1e-3 * tail + 1e-12)
+
+
+def test_fullsize_long_context_first_and_middle_keys():
+    # the importance call of the long-context batch (2 x 32768 tokens) as the benchmark makes it
+    # (preallocated workspace), checked on the first 256 keys and a 256-key block in the middle
+    # of prompt 0: every one of the prompt's 32768 rows reaches its first keys, so these are the
+    # longest column sums the kernel forms
+    w = synth.get_workload("long")
+    inp = I.make_inputs(w, 42)
+    cu = inp["cu_seqlens"].astype(np.int64)
+    n_tok, B, max_len = int(inp["n_tok"]), len(inp["lengths"]), int(inp["lengths"].max())
+    Hdn, K = w.head
+    Q, Kk, cud = dev(inp["Q"]), dev(inp["K"]), dev(inp["cu_seqlens"])
+    bufs = alloc_buffers(n_tok, B, max_len, w.d, w.V, w.L, w.Hq, w.Hkv, w.dh, Hdn, K, Q.device)
+    S = host(estp.attn_importance(Q, Kk, cud, max_len, S=bufs["S"], workspace=bufs["ws_importance"]))
+    del Q, Kk, cud, bufs
+    torch.cuda.empty_cache()
+    lo, hi = int(cu[0]), int(cu[1])
+    N = hi - lo
+    keys = np.concatenate([np.arange(256), np.arange(N // 2, N // 2 + 256)])
+    ref = _keys_by_head(inp["Q"][:, lo:hi], inp["K"][:, lo:hi], N, keys, w.Hq)
+    rel = np.abs(S[lo + keys] - ref) / ref
+    print(f"long prompt 0: keys 0-255 max rel dS = {rel[:256].max():.1e}, "
+          f"keys {N // 2}-{N // 2 + 255} max rel dS = {rel[256:].max():.1e}")
+    assert np.all(np.abs(S[lo + keys] - ref) <= 1e-3 * ref + 1e-12)
 
 
 def _torch_row_lse(Q, K, cu, scale):

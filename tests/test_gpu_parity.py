@@ -15,7 +15,7 @@ import oracle
 import paper_2608_15592_amd as estp
 import synth
 from synth import inputs as I
-from tests._util import check_argmax_margin, check_order_margin, dev, host, rel_l2
+from tests._util import check_argmax_margin, check_order_margin, check_vocab_argmax, dev, host, rel_l2
 
 pytestmark = pytest.mark.gpu
 
@@ -66,13 +66,44 @@ ENTROPY_CASES = [
 def test_entropy_parity(n_tok, d, V, std, tag):
     X = _hidden(n_tok, d, 1)
     W = _weight(V, d, 2, std)
-    H = host(estp.token_entropy(dev(X), dev(W)))
+    Xd, Wd = dev(X), dev(W)
+    H = host(estp.token_entropy(Xd, Wd))
     ref = oracle.token_entropy(X, W)
     err = np.abs(H - ref).max()
     print(f"{tag}: max |dH| = {err:.3e} nats (H in [{ref.min():.3f}, {ref.max():.3f}])")
     assert err <= H_TOL
     if std == 0.0:
         np.testing.assert_allclose(H, math.log(V), atol=H_TOL)
+    # the same call asked for the most probable next token as well: H unchanged bit for bit,
+    # the mode exact under the margin rule
+    am = torch.full((n_tok,), -7, dtype=torch.int32, device="cuda")
+    H2 = host(estp.token_entropy(Xd, Wd, vocab_argmax=am))
+    np.testing.assert_array_equal(H2, H)
+    am = host(am)
+    counts = check_vocab_argmax(am, X, W)
+    print(f"{tag}: vocab argmax exact on {counts['exact']} rows, near ties {counts['tie']}")
+    if std == 0.0:
+        assert np.all(am == 0)  # every logit exactly 0: the lowest index
+
+
+def test_entropy_argmax_exact_ties():
+    # copies of one strong row at several vocabulary positions tie exactly (identical operands give
+    # identical sums): the lowest position wins, in whichever tile, half or slice the copies land
+    n_tok, d, V = 300, 256, 9000
+    X = _hidden(n_tok, d, 7)
+    W = _weight(V, d, 8)
+    g = np.random.default_rng(9)
+    strong = _bf16(g.standard_normal(d).astype(np.float32) * 0.3)
+    for pos in (8700, 4100, 300, 129, 7000):
+        W[pos] = strong
+    am = torch.empty(n_tok, dtype=torch.int32, device="cuda")
+    estp.token_entropy(dev(X), dev(W), vocab_argmax=am)
+    am = host(am)
+    z = oracle.widen(X) @ oracle.widen(strong)
+    rows = z > (oracle.widen(X) @ oracle.widen(np.delete(W, [8700, 4100, 300, 129, 7000], axis=0)).T).max(axis=1) + 0.1
+    assert rows.sum() > 50
+    assert np.all(am[rows] == 129), np.unique(am[rows])
+    check_vocab_argmax(am, X, W)
 
 
 def test_entropy_late_peak():
