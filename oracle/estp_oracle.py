@@ -267,17 +267,18 @@ def attn_importance_keys(Q, K, N: int, keys, scale: Optional[float] = None, head
     that prompt alone.  ``heads`` restricts the head average of Eq. 1 to a
     subset of the query heads (each term still divided by Hq), so that the
     sums over a partition of the heads add up to S; default all heads.
-    Returns [len(keys)], summed over layers like ``attn_importance``.
+    Returns [len(keys)], summed over layers like ``attn_importance``.  Inputs
+    are widened one (layer, head) at a time, so long prompts stay in memory.
     """
-    Qd = widen(Q)
-    Kd = widen(K)
-    if Qd.ndim == 3:
-        Qd, Kd = Qd[None], Kd[None]
-    L, n, Hq, dh = Qd.shape
+    Q = np.asarray(Q)
+    K = np.asarray(K)
+    if Q.ndim == 3:
+        Q, K = Q[None], K[None]
+    L, n, Hq, dh = Q.shape
     keys = np.asarray(keys, dtype=np.int64)
     if n != N or keys.size == 0 or keys.min() < 0 or keys.max() >= N:
         raise ValueError("Q, K must hold exactly the prompt and every key must lie in [0, N)")
-    G = Hq // Kd.shape[2]
+    G = Hq // K.shape[2]
     if scale is None:
         scale = 1.0 / math.sqrt(dh)
     heads = range(Hq) if heads is None else heads
@@ -286,9 +287,11 @@ def attn_importance_keys(Q, K, N: int, keys, scale: Optional[float] = None, head
     for l in range(L):
         colsum = np.zeros(keys.size, dtype=np.float64)
         for h in heads:
+            q = widen(Q[l, :, h, :])
+            k = widen(K[l, :, h // G, :])
             for i0 in range(first, N, row_chunk):
                 i1 = min(N, i0 + row_chunk)
-                s = scale * (Qd[l, i0:i1, h, :] @ Kd[l, :i1, h // G, :].T)   # rows i0..i1-1, keys 0..i1-1
+                s = scale * (q[i0:i1] @ k[:i1].T)                # rows i0..i1-1, keys 0..i1-1
                 A = _causal_softmax_rows(s, i0)
                 colsum += _gather_cols(A, keys, i1) / Hq
         S += colsum / N
