@@ -115,6 +115,30 @@ ESTP_API int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int
                        float* H, int32_t* vocab_argmax, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Token entropy without allocation or workspace.
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  The same
+ * computation and kernels as estp_token_entropy (same arguments, same
+ * results bit for bit), but the per-slice partial states live in a device
+ * array owned by the library: ESTP_NOALLOC_SCRATCH_BYTES (32 MiB) on every
+ * GPU the library runs on, held until the process ends.  The call allocates
+ * nothing; the caller still passes X, W and the outputs.
+ *
+ *   A shape whose estp_token_entropy_workspace_size() exceeds
+ *   ESTP_NOALLOC_SCRATCH_BYTES returns ESTP_ERR_UNSUPPORTED before any device
+ *   work (with V >= 4096: n_tok up to 104857 tokens fit).
+ *   All calls on one GPU share its array, and it keeps the last call's
+ *   contents: calls that can overlap on one GPU (several streams, several
+ *   host threads) race and must be serialised by the caller.
+ *   ESTP_ERR_HIP if the runtime cannot give the array's address on the
+ *   current device.
+ * ------------------------------------------------------------------------ */
+#define ESTP_NOALLOC_SCRATCH_BYTES (32u << 20)
+ESTP_API int estp_token_entropy_noalloc(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
+                               float* H, int32_t* vocab_argmax, void* stream);
+
+/* ------------------------------------------------------------------------
  * Attention importance (Eq. 1, Section 4.1).
  *
  *   S[j] = sum_l (1/N_b) sum_{i>=j} (1/Hq) sum_h A^{l,h}_{ij}

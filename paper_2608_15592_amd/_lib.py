@@ -25,12 +25,13 @@ LIB_PATH = os.environ.get("ESTP_LIBRARY") or os.path.join(_HERE, "libestp.so")
 ESTP_OK, ESTP_ERR_INVALID_ARG, ESTP_ERR_UNSUPPORTED, ESTP_ERR_WORKSPACE, ESTP_ERR_HIP = range(5)
 ESTP_BF16, ESTP_F32 = 0, 1
 ESTP_IMPORTANCE_EXCLUDE_SELF = 1
+ESTP_NOALLOC_SCRATCH_BYTES = 32 << 20
 NORMS = {"none": 0, "zscore": 1, "minmax": 2}
 ACTS = {"relu": 0, "gelu_tanh": 1}
 
 EXPORTS = (
     "estp_version", "estp_status_string", "estp_last_error",
-    "estp_token_entropy_workspace_size", "estp_token_entropy",
+    "estp_token_entropy_workspace_size", "estp_token_entropy", "estp_token_entropy_noalloc",
     "estp_attn_importance_workspace_size", "estp_attn_importance",
     "estp_attn_importance_from_lse_workspace_size", "estp_attn_importance_from_lse",
     "estp_attn_importance_ex_workspace_size", "estp_attn_importance_ex",
@@ -75,6 +76,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_token_entropy_workspace_size.argtypes = [_I64, _I32, _I32, _INT]
     lib.estp_token_entropy.restype = _INT
     lib.estp_token_entropy.argtypes = [_P, _P, _I64, _I32, _I32, _INT, _P, _P, _P, _SZ, _P]
+    lib.estp_token_entropy_noalloc.restype = _INT
+    lib.estp_token_entropy_noalloc.argtypes = [_P, _P, _I64, _I32, _I32, _INT, _P, _P, _P]
     lib.estp_attn_importance_workspace_size.restype = _SZ
     lib.estp_attn_importance_workspace_size.argtypes = [_I64, _I32, _I32, _I32, _I32, _I32, _I32, _INT]
     lib.estp_attn_importance.restype = _INT
@@ -204,6 +207,27 @@ def token_entropy(X: torch.Tensor, W: torch.Tensor, H: Optional[torch.Tensor] = 
         workspace, wsb = _workspace(lib.estp_token_entropy_workspace_size(n_tok, d, V, dt), X.device, workspace)
         _check(lib.estp_token_entropy(_ptr(X), _ptr(W), n_tok, d, V, dt, _ptr(H), _ptr(vocab_argmax),
                                       _ptr(workspace), wsb, st), "estp_token_entropy")
+    return H
+
+
+def token_entropy_noalloc(X: torch.Tensor, W: torch.Tensor, H: torch.Tensor,
+                          vocab_argmax: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """``token_entropy`` through estp_token_entropy_noalloc: the library's own per-GPU scratch
+    instead of a workspace, so the call allocates nothing (H and the optional ``vocab_argmax``
+    are the caller's).  Calls that overlap on one GPU race on that scratch."""
+    lib = load()
+    _need(X, "X", ndim=2)
+    _need(W, "W", device=X.device, dtype=X.dtype, ndim=2)
+    n_tok, d = X.shape
+    V = W.shape[0]
+    if W.shape[1] != d:
+        raise ValueError("X and W disagree on d")
+    _sized(H, "H", n_tok, device=X.device, dtype=torch.float32)
+    if vocab_argmax is not None:
+        _sized(vocab_argmax, "vocab_argmax", n_tok, device=X.device, dtype=torch.int32)
+    with _on(stream, X.device) as st:
+        _check(lib.estp_token_entropy_noalloc(_ptr(X), _ptr(W), n_tok, d, V, _dtype_code(X), _ptr(H),
+                                              _ptr(vocab_argmax), st), "estp_token_entropy_noalloc")
     return H
 
 

@@ -39,6 +39,9 @@
 // 16 x 16: concurrent workgroups stream the same W and X tiles through that
 // XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices that
 // hold one tile more than the others are spread over the XCDs.
+#include <atomic>
+#include <mutex>
+
 #include "estp_common.h"
 #include "f32_paths.h"
 
@@ -547,39 +550,39 @@ extern "C" size_t estp_token_entropy_workspace_size(int64_t n_tok, int32_t d, in
   return c.bytes();
 }
 
-extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
-                                  float* H, int32_t* vocab_argmax, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
-  clear_error();
-  ESTP_REQUIRE(X && W && H, ESTP_ERR_INVALID_ARG, "estp_token_entropy: X, W and H must be non-null");
-  ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: n_tok must be in [1, 2^31), got %lld", (long long)n_tok);
-  ESTP_REQUIRE(V >= 1, ESTP_ERR_INVALID_ARG, "estp_token_entropy: V must be >= 1, got %d", V);
-  ESTP_REQUIRE(d >= 8 && d % 8 == 0, ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: d must be a positive multiple of 8, got %d", d);
-  ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: unknown dtype %d", dtype);
-  ESTP_REQUIRE(dtype == ESTP_F32 || d % 32 == 0, ESTP_ERR_UNSUPPORTED,
-               "estp_token_entropy: d must be a multiple of 32 for the matrix-core path, got %d", d);
-  ESTP_REQUIRE(size_t(d) * 2 * kBV < (size_t(1) << 32), ESTP_ERR_UNSUPPORTED,
-               "estp_token_entropy: d = %d too large", d);
-  ESTP_REQUIRE(aligned(X, 16) && aligned(W, 16), ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: X and W must be 16-byte aligned");
-  ESTP_REQUIRE(aligned(H, 4) && aligned(vocab_argmax, 4), ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: H and vocab_argmax must be 4-byte aligned");
-  const size_t need = estp_token_entropy_workspace_size(n_tok, d, V, dtype);
-  ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
-               "estp_token_entropy: workspace of %zu bytes, %zu needed", workspace_bytes, need);
-  ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
-               "estp_token_entropy: workspace must be non-null and 256-byte aligned");
+namespace {
 
+// Host-side checks shared by both entry points; `fn` names the caller in the error message.
+int check_entropy_args(const char* fn, const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V,
+                       int dtype, const float* H, const int32_t* vocab_argmax) {
+  ESTP_REQUIRE(X && W && H, ESTP_ERR_INVALID_ARG, "%s: X, W and H must be non-null", fn);
+  ESTP_REQUIRE(n_tok >= 1 && n_tok <= INT32_MAX, ESTP_ERR_INVALID_ARG, "%s: n_tok must be in [1, 2^31), got %lld", fn,
+               (long long)n_tok);
+  ESTP_REQUIRE(V >= 1, ESTP_ERR_INVALID_ARG, "%s: V must be >= 1, got %d", fn, V);
+  ESTP_REQUIRE(d >= 8 && d % 8 == 0, ESTP_ERR_INVALID_ARG, "%s: d must be a positive multiple of 8, got %d", fn, d);
+  ESTP_REQUIRE(dtype == ESTP_BF16 || dtype == ESTP_F32, ESTP_ERR_INVALID_ARG, "%s: unknown dtype %d", fn, dtype);
+  ESTP_REQUIRE(dtype == ESTP_F32 || d % 32 == 0, ESTP_ERR_UNSUPPORTED,
+               "%s: d must be a multiple of 32 for the matrix-core path, got %d", fn, d);
+  ESTP_REQUIRE(size_t(d) * 2 * kBV < (size_t(1) << 32), ESTP_ERR_UNSUPPORTED, "%s: d = %d too large", fn, d);
+  ESTP_REQUIRE(aligned(X, 16) && aligned(W, 16), ESTP_ERR_INVALID_ARG, "%s: X and W must be 16-byte aligned", fn);
+  ESTP_REQUIRE(aligned(H, 4) && aligned(vocab_argmax, 4), ESTP_ERR_INVALID_ARG,
+               "%s: H and vocab_argmax must be 4-byte aligned", fn);
   const int n = int(n_tok);
+  const int n_vsplit = choose_vsplit((V + kBV - 1) / kBV);
+  const size_t n_wg =
+      dtype == ESTP_F32 ? entropy_f32_workgroups(n, n_vsplit) : size_t(n_vsplit) * size_t((n + kBT - 1) / kBT);
+  ESTP_REQUIRE(fits_launch(n_wg, kWaves * 64), ESTP_ERR_UNSUPPORTED,
+               "%s: n_tok = %d needs %zu workgroups, more than one launch holds", fn, n, n_wg);
+  return ESTP_OK;
+}
+
+// The kernels of one call on checked arguments; `workspace` holds
+// estp_token_entropy_workspace_size() bytes, 256-byte aligned.
+int launch_token_entropy(const void* X, const void* W, int n, int d, int V, int dtype, float* H,
+                         int32_t* vocab_argmax, void* workspace, hipStream_t s) {
   const int n_vt = (V + kBV - 1) / kBV;
   const int n_tt = (n + kBT - 1) / kBT;
   const int n_vsplit = choose_vsplit(n_vt);
-  const size_t n_wg = dtype == ESTP_F32 ? entropy_f32_workgroups(n, n_vsplit) : size_t(n_vsplit) * n_tt;
-  ESTP_REQUIRE(fits_launch(n_wg, kWaves * 64), ESTP_ERR_UNSUPPORTED,
-               "estp_token_entropy: n_tok = %d needs %zu workgroups, more than one launch holds", n, n_wg);
   Carver c(workspace);
   float* pm = c.take<float>(size_t(n_vsplit) * n);
   float* ps = c.take<float>(size_t(n_vsplit) * n);
@@ -587,11 +590,10 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
   float* pz = c.take<float>(size_t(n_vsplit) * n);
   int* pa = c.take<int>(size_t(n_vsplit) * n);
   const bool want_arg = vocab_argmax != nullptr;
-  hipStream_t s = static_cast<hipStream_t>(stream);
 
   if (dtype == ESTP_F32) {
-    launch_entropy_f32(static_cast<const float*>(X), static_cast<const float*>(W), n, int(d), int(V), n_vsplit, pm,
-                       ps, pt, pz, want_arg ? pa : nullptr, s);
+    launch_entropy_f32(static_cast<const float*>(X), static_cast<const float*>(W), n, d, V, n_vsplit, pm, ps, pt, pz,
+                       want_arg ? pa : nullptr, s);
     ESTP_CHECK_LAUNCH("entropy_f32_kernel");
   } else {
     const dim3 grid(n_vsplit * n_tt), block(kWaves * 64);
@@ -599,18 +601,18 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
     const uint16_t* Wh = static_cast<const uint16_t*>(W);
     if (d % 64 == 0) {
       if (want_arg)
-        entropy_gemm_kernel<5, 64, true><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
-                                                                ps, pt, pz, pa);
+        entropy_gemm_kernel<5, 64, true><<<grid, block, 0, s>>>(Xh, Wh, n, d, V, n_vsplit, n_vt, n_tt, pm, ps, pt, pz,
+                                                                pa);
       else
-        entropy_gemm_kernel<5, 64, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
-                                                                 ps, pt, nullptr, nullptr);
+        entropy_gemm_kernel<5, 64, false><<<grid, block, 0, s>>>(Xh, Wh, n, d, V, n_vsplit, n_vt, n_tt, pm, ps, pt,
+                                                                 nullptr, nullptr);
     } else {
       if (want_arg)
-        entropy_gemm_kernel<9, 32, true><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
-                                                                ps, pt, pz, pa);
+        entropy_gemm_kernel<9, 32, true><<<grid, block, 0, s>>>(Xh, Wh, n, d, V, n_vsplit, n_vt, n_tt, pm, ps, pt, pz,
+                                                                pa);
       else
-        entropy_gemm_kernel<9, 32, false><<<grid, block, 0, s>>>(Xh, Wh, n, int(d), int(V), n_vsplit, n_vt, n_tt, pm,
-                                                                 ps, pt, nullptr, nullptr);
+        entropy_gemm_kernel<9, 32, false><<<grid, block, 0, s>>>(Xh, Wh, n, d, V, n_vsplit, n_vt, n_tt, pm, ps, pt,
+                                                                 nullptr, nullptr);
     }
     ESTP_CHECK_LAUNCH("entropy_gemm_kernel");
   }
@@ -618,4 +620,80 @@ extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, i
                                                                    n_vsplit, H, vocab_argmax);
   ESTP_CHECK_LAUNCH("entropy_merge_kernel");
   return ESTP_OK;
+}
+
+}  // namespace
+
+extern "C" int estp_token_entropy(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V, int dtype,
+                                  float* H, int32_t* vocab_argmax, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  clear_error();
+  const int st = check_entropy_args("estp_token_entropy", X, W, n_tok, d, V, dtype, H, vocab_argmax);
+  if (st != ESTP_OK) return st;
+  const size_t need = estp_token_entropy_workspace_size(n_tok, d, V, dtype);
+  ESTP_REQUIRE(workspace_bytes >= need, ESTP_ERR_WORKSPACE,
+               "estp_token_entropy: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  ESTP_REQUIRE(workspace && aligned(workspace, 256), ESTP_ERR_INVALID_ARG,
+               "estp_token_entropy: workspace must be non-null and 256-byte aligned");
+  return launch_token_entropy(X, W, int(n_tok), d, V, dtype, H, vocab_argmax, workspace,
+                              static_cast<hipStream_t>(stream));
+}
+
+
+// ------------------------------------------------------------------ no-allocation variant
+//
+// The per-slice partial states of estp_token_entropy_noalloc live in this
+// file-scope device array instead of a caller workspace.  Every GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// the array's name is only a stand-in: the device address of the current
+// GPU's copy comes from hipGetSymbolAddress, looked up once per device and
+// kept; kernels and copies only ever see that address.  Every partial is
+// written before it is read, so nothing has to be cleared between calls;
+// calls that overlap on one GPU share the array and race.
+static_assert(ESTP_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size");
+static __device__ __align__(256) char scratch[ESTP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current GPU's `scratch` (nullptr and an error message on failure).
+void* scratch_of_current_device(const char* fn) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_error("%s: no usable current HIP device (%d)", fn, dev);
+    return nullptr;
+  }
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_error("%s: hipGetSymbolAddress of the scratch array on device %d: %s", fn, dev, hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
+}  // namespace
+
+extern "C" int estp_token_entropy_noalloc(const void* X, const void* W, int64_t n_tok, int32_t d, int32_t V,
+                                          int dtype, float* H, int32_t* vocab_argmax, void* stream) {
+  clear_error();
+  const char* fn = "estp_token_entropy_noalloc";
+  const int st = check_entropy_args(fn, X, W, n_tok, d, V, dtype, H, vocab_argmax);
+  if (st != ESTP_OK) return st;
+  const size_t need = estp_token_entropy_workspace_size(n_tok, d, V, dtype);
+  ESTP_REQUIRE(need <= size_t(ESTP_NOALLOC_SCRATCH_BYTES), ESTP_ERR_UNSUPPORTED,
+               "%s: n_tok = %lld with V = %d needs %zu bytes of scratch, more than the %zu the library holds per "
+               "GPU; call estp_token_entropy with a workspace instead",
+               fn, (long long)n_tok, V, need, size_t(ESTP_NOALLOC_SCRATCH_BYTES));
+  void* ws = scratch_of_current_device(fn);
+  if (!ws) return ESTP_ERR_HIP;
+  return launch_token_entropy(X, W, int(n_tok), d, V, dtype, H, vocab_argmax, ws, static_cast<hipStream_t>(stream));
 }

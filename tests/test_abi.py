@@ -71,6 +71,31 @@ def test_entropy_validation():
 
 
 @needs_no_gpu
+def test_entropy_noalloc_validation():
+    # the no-allocation variant refuses, on the host, the same invalid arguments and every shape
+    # whose partial states exceed the library's scratch (its size is in the header)
+    lib = estp.load()
+    limit = _lib.ESTP_NOALLOC_SCRATCH_BYTES
+    assert re.search(r"#define ESTP_NOALLOC_SCRATCH_BYTES \(32u << 20\)", open(HEADER).read())
+    assert limit == 32 << 20
+    n_big = limit // (5 * 16 * 4) + 1
+    assert lib.estp_token_entropy_workspace_size(n_big, 32, 4096, 0) > limit
+    cases = [
+        ((None, FAKE, 100, 64, 1000, 0, FAKE, None, None), 1),               # null X
+        ((FAKE, FAKE, 100, 60, 1000, 0, FAKE, None, None), 1),               # d % 8
+        ((FAKE, FAKE, 100, 40, 1000, 0, FAKE, None, None), 2),               # bf16 d % 32
+        ((FAKE, FAKE, 100, 64, 1000, 0, FAKE, UNALIGNED, None), 1),          # argmax alignment
+        ((FAKE, FAKE, n_big, 32, 4096, 0, FAKE, None, None), 2),             # past the scratch
+        ((FAKE, FAKE, 4 * n_big, 32, 1000, 1, FAKE, FAKE, None), 2),         # fp32, 4 slices, past it
+    ]
+    for args, code in cases:
+        assert lib.estp_token_entropy_noalloc(*args) == code, (args, lib.estp_last_error())
+        assert lib.estp_last_error()
+    lib.estp_token_entropy_noalloc(FAKE, FAKE, n_big, 32, 4096, 0, FAKE, None, None)
+    assert b"scratch" in lib.estp_last_error()
+
+
+@needs_no_gpu
 def test_importance_validation():
     lib = estp.load()
     ws = lib.estp_attn_importance_workspace_size(100, 2, 60, 1, 4, 2, 64, 0)
