@@ -303,8 +303,8 @@ ESTP_API int estp_head_train_step(const float* pooled, const float* y, int32_t B
  * estp_misalignment: the entropy / semantics split behind Fig. 1b
  * (Section 1).  Within each prompt (N tokens) the tokens are ranked by H and
  * by S (ascending; equal values by token index) and split into the lowest
- * floor(frac_low N) and the highest floor(frac_high N) (the paper's 60th
- * percentile split is frac_low = frac_high = 0.4).
+ * floor(frac_low N) and the highest floor(frac_high N) (Fig. 1b compares
+ * the top and bottom 40%: frac_low = frac_high = 0.4).
  *   H, S [n_tok]    float32, device;  cu_seqlens [B+1] int32, device
  *   counts [B, 4]   int32 output: #high-H, #high-H that are low-S,
  *                   #low-H, #low-H that are high-S
