@@ -57,8 +57,8 @@ def cpu_baseline(inp, lam1, lam2, alpha, norm, n_prompts: int):
     t0 = time.perf_counter()
     reps = 0
     while True:  # a sample that runs in well under a second is repeated, for a stable rate
-        oracle.run_path(inp["X"][:n], inp["W"], inp["Q"][:, :n], inp["K"][:, :n], cu_s, lam1, lam2, alpha, norm,
-                        head=(inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"]))
+        ref = oracle.run_path(inp["X"][:n], inp["W"], inp["Q"][:, :n], inp["K"][:, :n], cu_s, lam1, lam2, alpha,
+                              norm, head=(inp["W1"], inp["b1"], inp["W2"], inp["b2"], inp["centres"]))
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= 2.0:
@@ -71,7 +71,60 @@ def cpu_baseline(inp, lam1, lam2, alpha, norm, n_prompts: int):
         "sample": (f"the first {n_prompts} whole prompts of the workload ({n} tokens), whole path"
                    + (f", {reps} times" if reps > 1 else "") + f", {dt:.1f} s"),
         "host_cpus": len(os.sched_getaffinity(0)),
-    }
+    }, ref, n_prompts
+
+
+def parity_of_run(ref, n_prompts: int, got: dict) -> dict:
+    """This run's own outputs on the oracle's sample (its first whole prompts) against the oracle:
+    the errors the parity tests bound (|dH| <= 2e-3 nats, |dS| <= 1e-3 S, pooled relative L2
+    <= 1e-3, y-hat relative 1e-3)."""
+    n = len(ref["H"])
+    dH = float(np.abs(got["H"][:n] - ref["H"]).max())
+    dS = float((np.abs(got["S"][:n] - ref["S"]) / ref["S"]).max())
+    pooled = got["pooled"][:n_prompts].astype(np.float64)
+    dP = float(max(np.linalg.norm(pooled[b] - ref["pooled"][b]) / np.linalg.norm(ref["pooled"][b])
+                   for b in range(n_prompts)))
+    dY = float((np.abs(got["yhat"][:n_prompts] - ref["yhat"]) / np.maximum(np.abs(ref["yhat"]), 1e-30)).max())
+    return {"sample": f"first {n_prompts} prompts ({n} tokens)", "max_abs_dH_nats": dH, "max_rel_dS": dS,
+            "max_pooled_rel_l2": dP, "max_yhat_rel": dY,
+            # both sides index tokens from 0 on this sample; near ties may differ (margin rule)
+            "top_token_agree": f"{int((got['top'][:n_prompts] == np.asarray(ref['top'])).sum())}/{n_prompts}",
+            "within_bounds": bool(dH <= 2e-3 and dS <= 1e-3 and dP <= 1e-3 and dY <= 1e-3)}
+
+
+def source_hash() -> str:
+    """sha256 (16 hex digits) of the library sources, the header and this script."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2608_15592_amd", "csrc", "*")))
+    files += [os.path.join(ROOT, "include", "estp.h"), os.path.abspath(__file__)]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def build_info(torch) -> dict:
+    """Where the numbers were taken: device, runtime versions, source revision."""
+    import subprocess
+    props = torch.cuda.get_device_properties(0)
+    rocm = None
+    for f in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        try:
+            rocm = open(f).read().strip()
+            break
+        except OSError:
+            pass
+    try:
+        head = subprocess.run(["git", "-C", ROOT, "rev-parse", "HEAD"], capture_output=True, text=True,
+                              timeout=10).stdout.strip() or None
+    except Exception:
+        head = None
+    return {"name": torch.cuda.get_device_name(0), "gcnArchName": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count, "hbm_bytes": props.total_memory,
+            "rocm": rocm, "hip_runtime": torch.version.hip, "torch": torch.__version__,
+            "source_sha256_16": source_hash(), "git_head": head}
 
 
 def _entropy_source_hash() -> str:
@@ -382,6 +435,36 @@ def main() -> int:
     copy_gbps = 2 * X.numel() * X.element_size() / (copy_ms * 1e-3) / 1e9
     del Xc
 
+    # The pooling call with cold caches: 1 GiB streamed through the caches before every
+    # repetition, each call bracketed on its own (median of 5).  Read-flushed: a reduction over
+    # the buffer leaves only clean lines, so the 256 MB MALL and the L2s hold none of X, H, S
+    # and nothing is waiting to be written back.  Write-flushed: a fill of the buffer instead,
+    # whose dirty lines (up to the MALL's 256 MB) are written back while the call reads X.
+    flush = torch.zeros(1 << 28, dtype=torch.float32, device=X.device)
+    torch.cuda.synchronize()
+
+    def cold_pool(refill):
+        times = []
+        for k in range(6):
+            if refill:
+                flush.fill_(float(k))
+            else:
+                flush.sum()
+            c0, c1 = HipEvent(), HipEvent()
+            c0.record(stream)
+            estp.combine_pool(X, bufs["S"], bufs["H"], cu, max_len, args.lambda1, args.lambda2, args.alpha,
+                              args.norm, pooled=bufs["pooled"], e=bufs["e"], top=bufs["top"],
+                              workspace=bufs["ws_pool"], stream=stream)
+            c1.record(stream)
+            torch.cuda.synchronize()
+            if k:
+                times.append(c0.elapsed_time(c1))
+        return float(np.median(times))
+
+    cold_ms = cold_pool(refill=False)
+    cold_w_ms = cold_pool(refill=True)
+    del flush
+
     ent_flop = 2.0 * n_tok * w.V * w.d
     imp_flop_alg = float(sum(int(T) * int(T) for T in inp["lengths"])) * w.dh * w.Hq * w.L  # one causal QK^T
     imp_exps = 2.0 * float(sum(int(T) * (int(T) + 1) // 2 for T in inp["lengths"])) * w.Hq * w.L  # two passes
@@ -449,17 +532,27 @@ def main() -> int:
         "pooling": {"bound": "hbm", "alg_bytes": pool_bytes, "achieved": pool_gbps, "peak": PEAK_HBM_GBPS,
                     "unit": "GB/s", "frac": pool_gbps / PEAK_HBM_GBPS,
                     "device_copy_GBps": copy_gbps, "frac_of_device_copy": pool_gbps / copy_gbps,
-                    "note": "whole combine_pool call (weights + pooling + chunk reduction); X is not cache "
-                            "resident (importance streams 2.7 GB of Q and K just before); device copy counts "
+                    "cold_mall_ms": cold_ms, "cold_mall_GBps": pool_bytes / (cold_ms * 1e-3) / 1e9,
+                    "cold_mall_frac": pool_bytes / (cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+                    "after_write_flush_ms": cold_w_ms,
+                    "after_write_flush_GBps": pool_bytes / (cold_w_ms * 1e-3) / 1e9,
+                    "note": "whole combine_pool call (weights + pooling); in the step, X is not cache resident "
+                            "(importance streams Q and K just before); cold_mall_*: median of 5 calls, each after "
+                            "a 1 GiB read that evicts everything with clean lines; after_write_flush_*: each after a "
+                            "1 GiB write, whose dirty lines are written back during the call; device copy counts "
                             "read + write bytes"},
-        "device": torch.cuda.get_device_name(0),
+        "device": build_info(torch),
         **({"graph": graph_info} if graph_info else {}),
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host sample ...")
-        result["cpu_baseline"] = cpu_baseline(inp, args.lambda1, args.lambda2, args.alpha, args.norm,
-                                              args.cpu_sample_prompts)
+        result["cpu_baseline"], ref, n_ref = cpu_baseline(inp, args.lambda1, args.lambda2, args.alpha, args.norm,
+                                                          args.cpu_sample_prompts)
         log(f"oracle: {result['cpu_baseline']['value']:.1f} tokens/s")
+        got = {k: bufs[k].cpu().numpy() for k in ("H", "S", "pooled", "top")}
+        got["yhat"] = yhat_s[0].cpu().numpy()
+        result["parity"] = parity_of_run(ref, n_ref, got)
+        log(f"parity of this run on the oracle sample: {result['parity']}")
     print(json.dumps(result), flush=True)
     return 0
 

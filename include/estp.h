@@ -84,6 +84,17 @@ ESTP_API const char* estp_status_string(int status);
 /* Detail of the last failed call on this thread ("" if none). */
 ESTP_API const char* estp_last_error(void);
 
+/* 1 when the debug checks are on in this process, else 0.  They are switched
+ * on by ESTP_DEBUG_CHECKS=1 in the environment (read once).  Every call that
+ * takes cu_seqlens then copies it back and checks it before any kernel runs
+ * (cu_seqlens[0] = 0, cu_seqlens[B] = n_tok, every prompt length in
+ * [1, max_seqlen]; ESTP_ERR_INVALID_ARG otherwise), and every call that
+ * builds a work list of live blocks or chunks on the device compares it with
+ * its definition before the kernels that use it run (ESTP_ERR_HIP on a
+ * mismatch).  The checks synchronise the stream: for testing, not for use
+ * under graph capture. */
+ESTP_API int estp_debug_checks(void);
+
 /* ------------------------------------------------------------------------
  * Token entropy (Eq. 2, Section 4.2).
  *

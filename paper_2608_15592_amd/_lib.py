@@ -30,7 +30,7 @@ NORMS = {"none": 0, "zscore": 1, "minmax": 2}
 ACTS = {"relu": 0, "gelu_tanh": 1}
 
 EXPORTS = (
-    "estp_version", "estp_status_string", "estp_last_error",
+    "estp_version", "estp_status_string", "estp_last_error", "estp_debug_checks",
     "estp_token_entropy_workspace_size", "estp_token_entropy", "estp_token_entropy_noalloc",
     "estp_attn_importance_workspace_size", "estp_attn_importance",
     "estp_attn_importance_from_lse_workspace_size", "estp_attn_importance_from_lse",
@@ -72,6 +72,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.estp_status_string.argtypes = [_INT]
     lib.estp_last_error.restype = ctypes.c_char_p
     lib.estp_last_error.argtypes = []
+    lib.estp_debug_checks.restype = _INT
+    lib.estp_debug_checks.argtypes = []
     lib.estp_token_entropy_workspace_size.restype = _SZ
     lib.estp_token_entropy_workspace_size.argtypes = [_I64, _I32, _I32, _INT]
     lib.estp_token_entropy.restype = _INT

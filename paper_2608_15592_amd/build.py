@@ -43,10 +43,31 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
-    """Compile every HIP source into one shared library; returns its path."""
+# Host code only, AddressSanitizer: every -fsanitize flag sits behind -Xarch_host, so the gfx950
+# device code is built exactly as in the plain library.  The runtime is linked dynamically; a
+# process that loads this library (Python included) needs it preloaded: see asan_runtime().
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer",
+              "-Xarch_host", "-shared-libsan", "-Xarch_host", "-g"]
+ASAN_LIB = os.path.join(HERE, "libestp_asan.so")
+
+
+def asan_runtime() -> str:
+    """Path of the AddressSanitizer runtime that hipcc's clang links against."""
+    res = subprocess.run([hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = res.stdout.strip()
+    if res.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("AddressSanitizer runtime not found")
+    return path
+
+
+def build(verbose: bool = False, out: str = LIB, defines=(), sanitize: bool = False) -> str:
+    """Compile every HIP source into one shared library; returns its path.  ``sanitize`` adds
+    AddressSanitizer to the host code (default output libestp_asan.so)."""
+    if sanitize and out == LIB:
+        out = ASAN_LIB
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *[f"-D{d}" for d in defines], f"-I{INCLUDE}", f"-I{CSRC}", *sources(), "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *(ASAN_FLAGS if sanitize else []), *[f"-D{d}" for d in defines], f"-I{INCLUDE}",
+           f"-I{CSRC}", *sources(), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -58,4 +79,4 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, sanitize=os.environ.get("ASAN") == "1"))

@@ -172,6 +172,11 @@ extern "C" int estp_misalignment(const float* H, const float* S, const int32_t* 
                "estp_misalignment: fractions must be in [0, 1]");
   ESTP_REQUIRE(fits_launch(size_t(B), kAThreads), ESTP_ERR_UNSUPPORTED,
                "estp_misalignment: B = %d is more than one launch holds", B);
+  if (debug_checks_enabled()) {
+    const int st = debug_check_cu("estp_misalignment", cu_seqlens, B, -1, INT32_MAX, static_cast<hipStream_t>(stream),
+                                  nullptr);
+    if (st != ESTP_OK) return st;
+  }
   misalignment_kernel<<<dim3(B), dim3(kAThreads), 0, static_cast<hipStream_t>(stream)>>>(H, S, cu_seqlens, frac_low,
                                                                                          frac_high, counts);
   ESTP_CHECK_LAUNCH("misalignment_kernel");

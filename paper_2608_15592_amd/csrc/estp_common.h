@@ -7,6 +7,8 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include <vector>
+
 #include "estp.h"
 
 namespace estp {
@@ -131,6 +133,17 @@ __device__ __forceinline__ Ent2 ent2_merge(Ent2 a, Ent2 b) {
 
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();
+
+// Debug mode: ESTP_DEBUG_CHECKS=1 in the environment (read once per process).  Calls that take
+// cu_seqlens copy it back and check it before any kernel runs (cu[0] = 0, cu[B] = n_tok, every
+// prompt length in [1, max_seqlen]); calls that build a work list on the device copy it back
+// and compare it with its definition before the kernels that consume it are launched.  Both
+// synchronise the stream, so the mode is for testing, not for graph capture.
+bool debug_checks_enabled();
+// n_tok < 0: the call does not state n_tok, cu_seqlens[B] is not compared.
+int debug_check_cu(const char* fn, const int32_t* cu_dev, int32_t B, int64_t n_tok, int32_t max_seqlen,
+                   hipStream_t s, std::vector<int>* cu_out);
+int debug_check_list(const char* fn, const int2* list_dev, const std::vector<int2>& expect, hipStream_t s);
 
 // Compute units of the current device (cached per device; 0 when the runtime cannot tell).
 constexpr int kMaxDevices = 64;

@@ -22,6 +22,8 @@
 // bitwise reproducible.  Both passes are register-bounded to three waves per
 // SIMD (168 VGPRs, no spills) so that one wave's exponentials overlap the
 // others' matrix-core work.
+#include <algorithm>
+
 #include "estp_common.h"
 #include "f32_paths.h"
 
@@ -453,16 +455,38 @@ __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restric
   S[base + j] = v / (float(N) * float(Hq));
 }
 
+// The definition block_list_kernel follows, on the host (debug checks): (prompt, block) for
+// every block index from the last down, prompts ascending within it, then (-1, 0) fill.
+std::vector<int2> block_list_on_host(const std::vector<int>& cu, int B, int nblk, size_t n_bound) {
+  std::vector<int2> out;
+  for (int k = nblk - 1; k >= 0; --k)
+    for (int b = 0; b < B; ++b)
+      if (cu[b + 1] - cu[b] > k * kQBlock) out.push_back(make_int2(b, k));
+  out.resize(std::max(out.size(), n_bound), make_int2(-1, 0));
+  out.resize(n_bound);
+  return out;
+}
+
 template <int DH>
-void launch(const void* Qv, const void* Kv, bool f32, const int* cu, int B, int max_seqlen, int n_tok, int L, int Hq,
-            int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S, float* lse2,
-            float* part, int2* blist, hipStream_t s) {
+int launch(const char* fn, const void* Qv, const void* Kv, bool f32, const int* cu, int B, int max_seqlen, int n_tok,
+           int L, int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S,
+           float* lse2, float* part, int2* blist, hipStream_t s) {
   static_assert(kQBlock == kKBlock, "the two passes share one list of 256-row blocks");
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
   const size_t n_bound = block_bound(n_tok, B, max_seqlen);
   const bool use_list = use_block_list(n_tok, B, max_seqlen);
-  if (use_list) {
+  if (debug_checks_enabled()) {  // cu_seqlens before any kernel reads it
+    std::vector<int> cu_h;
+    const int st = debug_check_cu(fn, cu, B, n_tok, max_seqlen, s, &cu_h);
+    if (st != ESTP_OK) return st;
+    if (use_list) {
+      block_list_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu, B, nqb, int(n_bound), blist);
+      ESTP_CHECK_LAUNCH("block_list_kernel");
+      const int st2 = debug_check_list(fn, blist, block_list_on_host(cu_h, B, nqb, n_bound), s);
+      if (st2 != ESTP_OK) return st2;
+    }
+  } else if (use_list) {
     block_list_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu, B, nqb, int(n_bound), blist);
   }
   const int2* bl = use_list ? blist : nullptr;
@@ -494,6 +518,8 @@ void launch(const void* Qv, const void* Kv, bool f32, const int* cu, int B, int 
     for (int l = 0; l < L; ++l) lw.w[l] = layer_weights[l];
   attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L, Hkv, Hq,
                                                                              layer_weights ? 1 : 0, lw, S);
+  ESTP_CHECK_LAUNCH(fn);
+  return ESTP_OK;
 }
 
 }  // namespace detail
@@ -528,13 +554,19 @@ int check_importance_args(const char* fn, const void* Q, const void* K, const in
   return ESTP_OK;
 }
 
-void launch_dh(int dh, const void* q, const void* k, bool f32, const int* cu, int B, int max_seqlen, int n, int L,
-               int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* lw, float* S, float* lse2,
-               float* part, int2* blist, hipStream_t s) {
+int launch_dh(const char* fn, int dh, const void* q, const void* k, bool f32, const int* cu, int B, int max_seqlen,
+              int n, int L, int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* lw, float* S,
+              float* lse2, float* part, int2* blist, hipStream_t s) {
   switch (dh) {
-    case 32: launch<32>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
-    case 64: launch<64>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
-    default: launch<128>(q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part, blist, s); break;
+    case 32:
+      return launch<32>(fn, q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part,
+                        blist, s);
+    case 64:
+      return launch<64>(fn, q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part,
+                        blist, s);
+    default:
+      return launch<128>(fn, q, k, f32, cu, B, max_seqlen, n, L, Hq, Hkv, scale, lse_in, strict, lw, S, lse2, part,
+                         blist, s);
   }
 }
 
@@ -572,10 +604,8 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, nullptr, 0, nullptr, S, lse2, part, blist, static_cast<hipStream_t>(stream));
-  ESTP_CHECK_LAUNCH("estp_attn_importance");
-  return ESTP_OK;
+  return launch_dh("estp_attn_importance", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen, int(n_tok), L, Hq,
+                   Hkv, scale, nullptr, 0, nullptr, S, lse2, part, blist, static_cast<hipStream_t>(stream));
 }
 
 extern "C" size_t estp_attn_importance_from_lse_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen,
@@ -611,10 +641,9 @@ extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const
   Carver c(workspace);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, blist, static_cast<hipStream_t>(stream));
-  ESTP_CHECK_LAUNCH("estp_attn_importance_from_lse");
-  return ESTP_OK;
+  return launch_dh("estp_attn_importance_from_lse", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
+                   int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, blist,
+                   static_cast<hipStream_t>(stream));
 }
 
 extern "C" size_t estp_attn_importance_ex_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L,
@@ -650,9 +679,7 @@ extern "C" int estp_attn_importance_ex(const void* Q, const void* K, const float
   float* lse2 = lse ? nullptr : c.take<float>(size_t(L) * Hq * n_tok);
   float* part = c.take<float>(size_t(L) * Hkv * n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
-  launch_dh(dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
-            int(n_tok), L, Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S,
-            lse2, part, blist, static_cast<hipStream_t>(stream));
-  ESTP_CHECK_LAUNCH("estp_attn_importance_ex");
-  return ESTP_OK;
+  return launch_dh("estp_attn_importance_ex", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen, int(n_tok), L,
+                   Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S, lse2, part,
+                   blist, static_cast<hipStream_t>(stream));
 }

@@ -600,6 +600,11 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
   const float a1 = lambda1 / alpha, a2 = lambda2 / alpha;
   const float4* cf = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  std::vector<int> cu_h;  // debug checks: cu_seqlens on the host, checked before any kernel reads it
+  if (debug_checks_enabled()) {
+    const int st = debug_check_cu("estp_combine_pool", cu_seqlens, B, n_tok, max_seqlen, s, &cu_h);
+    if (st != ESTP_OK) return st;
+  }
   if (norm == ESTP_NORM_ZSCORE) {
     zscore_stats_kernel<<<dim3(B), dim3(1024), 0, s>>>(S, H, cu_seqlens, a1, a2, coef);
     ESTP_CHECK_LAUNCH("zscore_stats_kernel");
@@ -625,6 +630,15 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
   if (use_map) {
     chunk_map_kernel<<<dim3(1), dim3(1024), 0, s>>>(cu_seqlens, B, nch, int(n_bound), map);
     ESTP_CHECK_LAUNCH("chunk_map_kernel");
+    if (debug_checks_enabled()) {  // its definition: (prompt, chunk) in prompt order, then (-1, 0)
+      std::vector<int2> expect;
+      for (int b = 0; b < B; ++b)
+        for (int c = 0; c * kChunk < cu_h[b + 1] - cu_h[b]; ++c) expect.push_back(make_int2(b, c));
+      expect.resize(std::max(expect.size(), n_bound), make_int2(-1, 0));
+      expect.resize(n_bound);
+      const int st = debug_check_list("estp_combine_pool", map, expect, s);
+      if (st != ESTP_OK) return st;
+    }
   }
   const dim3 grid(unsigned(n_k * nslices));
   const int2* cmap = use_map ? map : nullptr;
