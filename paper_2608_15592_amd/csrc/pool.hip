@@ -12,11 +12,13 @@
 // which is exactly sum_i e_i x_i; it also writes the arg-max token and, when
 // asked, the normalised weights e.  With z-scored or min-max scaled inputs a
 // per-prompt statistics pass (zscore_stats_kernel, minmax_stats_kernel) runs
-// first and folds the scaling into u = a1 S + a2 H + c0.  Batches of
+// first and gives u = c1 (S - centre_S) + c2 (H - centre_H).  Batches of
 // equal-length prompts that fill the chip by themselves take one kernel
 // instead (pool_prompt_kernel: a workgroup streams a whole prompt for one
-// feature slice, so there are no chunk partials to combine).  No atomics:
-// results are bitwise reproducible.
+// feature slice, so there are no chunk partials to combine), and so do other
+// batches of prompts up to 8192 tokens (pool_ragged_kernel: the slice width
+// follows each prompt's length); the chunked pair serves longer prompts.  No
+// atomics: results are bitwise reproducible.
 #include <algorithm>
 
 #include "estp_common.h"
@@ -77,33 +79,49 @@ __device__ void block_argmax(float& v, int& idx, float* shv, int* shi) {
     }
 }
 
-// Per-prompt coefficients of u = a1 S + a2 H + c0 for z-scored inputs:
-// (lambda1 (S - mean_S) / (std_S + eps) + lambda2 (H - mean_H) / (std_H + eps)) / alpha.
+__device__ double block_sum_d(double v, double* sh) {
+  v = wave_sum_d(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  double r = 0.0;
+  const int nw = blockDim.x >> 6;
+  for (int i = 0; i < nw; ++i) r += sh[i];
+  return r;
+}
+
+// Per-prompt coefficients (c1, c2, centre_S, centre_H) of u = c1 (S - centre_S) + c2 (H - centre_H)
+// for z-scored inputs: (lambda1 (S - mean_S) / (std_S + eps) + lambda2 (H - mean_H) / (std_H + eps))
+// / alpha.  Mean and variance are taken in fp64, and the centre stays a separate term: when a
+// prompt's values are nearly equal, S - centre is then (nearly) exact and the fp32 rounding of the
+// centre shifts every u of the prompt alike, which the softmax ignores.  (Folding it into one
+// constant would cancel two large terms for std ~ 0.)
 __global__ __launch_bounds__(1024) void zscore_stats_kernel(const float* __restrict__ S, const float* __restrict__ H,
                                                             const int* __restrict__ cu, float a1, float a2,
                                                             float4* __restrict__ coef) {
-  __shared__ float sh[16];
+  __shared__ double sh[16];
   const int b = blockIdx.x;
   const int base = cu[b];
   const int N = cu[b + 1] - base;
-  float ss = 0.f, sv = 0.f;
+  double ss = 0.0, sv = 0.0;
   for (int i = threadIdx.x; i < N; i += blockDim.x) {
-    ss += S[base + i];
-    sv += H[base + i];
+    ss += double(S[base + i]);
+    sv += double(H[base + i]);
   }
-  const float ms = block_sum(ss, sh) / N;
-  const float mh = block_sum(sv, sh) / N;
-  float vs = 0.f, vh = 0.f;
+  const double ms = block_sum_d(ss, sh) / N;
+  const double mh = block_sum_d(sv, sh) / N;
+  double vs = 0.0, vh = 0.0;
   for (int i = threadIdx.x; i < N; i += blockDim.x) {
-    const float ds = S[base + i] - ms, dh = H[base + i] - mh;
+    const double ds = double(S[base + i]) - ms, dh = double(H[base + i]) - mh;
     vs += ds * ds;
     vh += dh * dh;
   }
-  const float sds = sqrtf(block_sum(vs, sh) / N);
-  const float sdh = sqrtf(block_sum(vh, sh) / N);
+  const double sds = sqrt(block_sum_d(vs, sh) / N);
+  const double sdh = sqrt(block_sum_d(vh, sh) / N);
   if (threadIdx.x == 0) {
-    const float c1 = a1 / (sds + kZEps), c2 = a2 / (sdh + kZEps);
-    coef[b] = make_float4(c1, c2, -(c1 * ms + c2 * mh), 0.f);
+    const double c1 = double(a1) / (sds + double(kZEps)), c2 = double(a2) / (sdh + double(kZEps));
+    coef[b] = make_float4(float(c1), float(c2), float(ms), float(mh));
   }
 }
 
@@ -119,8 +137,9 @@ __device__ float block_reduce_max(float v, float* sh) {
   return r;
 }
 
-// Per-prompt coefficients of u = a1 S + a2 H + c0 for min-max scaled inputs:
-// (lambda1 (S - min_S) / (max_S - min_S + eps) + lambda2 (H - min_H) / (max_H - min_H + eps)) / alpha.
+// Per-prompt coefficients (c1, c2, min_S, min_H) of u = c1 (S - min_S) + c2 (H - min_H) for min-max
+// scaled inputs: (lambda1 (S - min_S) / (max_S - min_S + eps) + lambda2 (H - min_H) / (max_H - min_H
+// + eps)) / alpha.
 __global__ __launch_bounds__(1024) void minmax_stats_kernel(const float* __restrict__ S, const float* __restrict__ H,
                                                             const int* __restrict__ cu, float a1, float a2,
                                                             float4* __restrict__ coef) {
@@ -142,7 +161,7 @@ __global__ __launch_bounds__(1024) void minmax_stats_kernel(const float* __restr
   nh = block_reduce_max(nh, sh);
   if (threadIdx.x == 0) {
     const float c1 = a1 / ((xs + ns) + kZEps), c2 = a2 / ((xh + nh) + kZEps);
-    coef[b] = make_float4(c1, c2, c1 * ns + c2 * nh, 0.f);
+    coef[b] = make_float4(c1, c2, -ns, -nh);
   }
 }
 
@@ -180,6 +199,11 @@ struct Row8<float> {  // 8 fp32 in two 16-byte loads
 
 __device__ __forceinline__ float4 coef_of(const float4* coef, int b, float a1, float a2) {
   return coef ? coef[b] : make_float4(a1, a2, 0.f, 0.f);
+}
+
+// u = c1 (S - centre_S) + c2 (H - centre_H) for coefficients (c1, c2, centre_S, centre_H)
+__device__ __forceinline__ float fused_score(const float4& cf, float s, float h) {
+  return fmaf(cf.x, s - cf.z, cf.y * (h - cf.w));
 }
 
 // Streams one chunk of X.  Every wave forms the chunk's weights by itself
@@ -243,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void pool_partial_kernel(const T* __restr
     u[q] = -INFINITY;
     if (r < nr) {
       const int i = base + r0 + r;
-      u[q] = fmaf(cf.x, S[i], fmaf(cf.y, H[i], cf.z));
+      u[q] = fused_score(cf, S[i], H[i]);
       if (u[q] > m) {  // rows visited in increasing order: strict keeps the first
         m = u[q];
         mi = r0 + r;
@@ -329,12 +353,12 @@ __global__ __launch_bounds__(kPromptThreads) void pool_prompt_kernel(
       if (k < n_first) v[k] = Row8<T>::load(xp + size_t(wave + kPromptWaves * k) * d);
   }
 
-  // u = a1 S + a2 H + c0 for every token of the prompt, the first arg-max, the exp-sum
+  // u = c1 (S - centre_S) + c2 (H - centre_H) for every token of the prompt, the first arg-max, the exp-sum
   const float4 cf = coef_of(coef, b, a1, a2);
   float m = -INFINITY;
   int mi = 0x7fffffff;
   for (int i = tid; i < N; i += kPromptThreads) {
-    const float u = fmaf(cf.x, S[base + i], fmaf(cf.y, H[base + i], cf.z));
+    const float u = fused_score(cf, S[base + i], H[base + i]);
     wts[i] = u;
     if (u > m) {  // increasing i: strict keeps the first
       m = u;
@@ -381,6 +405,177 @@ __global__ __launch_bounds__(kPromptThreads) void pool_prompt_kernel(
 #pragma unroll
     for (int w = 0; w < kPromptWaves; ++w) s += red[w][tid];
     pooled[size_t(b) * d + f] = s * invZ;
+  }
+}
+
+// One-kernel pooling of a ragged batch.  Work unit = (prompt, feature slice),
+// like pool_prompt_kernel, but the slice width follows the prompt's length so
+// that every unit streams about kRaggedUnitBytes of X: a short prompt takes
+// whole rows, a 4096-token one 128 of 4096 features.  Each unit sums all rows
+// of its prompt for its slice, so there are no partials and no second kernel.
+// The units of a prompt are consecutive; a workgroup finds its (prompt, slice)
+// by scanning the prompt lengths itself (no list kernel).  G = F / 8 lanes
+// cover one row (16-byte loads), 512 / G rows are in flight per load round and
+// 8 rounds per thread; the row groups' sums are added in a fixed order.
+constexpr int kRaggedThreads = 512;
+constexpr int kRaggedMaxPrompts = 8192;  // prompts the in-kernel scan covers (16 per thread)
+constexpr int kRaggedMinSlice = 64;      // narrowest slice: 128-byte bf16 rows
+#ifndef ESTP_RAGGED_MAX_UNIT_BYTES
+#define ESTP_RAGGED_MAX_UNIT_BYTES (size_t(512) << 10)
+#endif
+#ifndef ESTP_RAGGED_ALIGN
+#define ESTP_RAGGED_ALIGN 64
+#endif
+constexpr size_t kRaggedMaxUnitBytes = ESTP_RAGGED_MAX_UNIT_BYTES;
+constexpr size_t kRaggedMinUnitBytes = size_t(64) << 10;
+constexpr int kRaggedAlign = ESTP_RAGGED_ALIGN;  // slice widths are multiples of this many features
+
+// Width of one of ns slices of d features, a multiple of kRaggedAlign (at least the 8 of a
+// 16-byte bf16 load), and never more than the workgroup covers.
+__host__ __device__ __forceinline__ int ragged_width(int d, int ns) {
+  const int w = ((d + ns - 1) / ns + kRaggedAlign - 1) / kRaggedAlign * kRaggedAlign;
+  return w < kRaggedThreads * 8 ? w : ((d + ns - 1) / ns + 7) / 8 * 8;
+}
+
+// Fewest slices whose width fits the workgroup (512 lanes x 8 features).
+__host__ __device__ __forceinline__ int ragged_min_slices(int d) {
+  int ns = 1;
+  while (ragged_width(d, ns) > kRaggedThreads * 8) ns *= 2;
+  return ns;
+}
+
+// Slice width for a prompt of n rows: d split into about (its X bytes) / unit_bytes slices, at
+// least ragged_min_slices(d), none narrower than kRaggedMinSlice features.
+__host__ __device__ __forceinline__ int ragged_slice_width(int n, int d, int elem_bytes, size_t unit_bytes) {
+  const size_t bytes = size_t(n) * size_t(d) * size_t(elem_bytes);
+  const size_t lo = size_t(ragged_min_slices(d)), hi = std::max(lo, size_t(d / kRaggedMinSlice));
+  return ragged_width(d, int(std::min(hi, std::max(lo, bytes / unit_bytes))));
+}
+
+// Units (nonempty slices) of a prompt of n rows.
+__host__ __device__ __forceinline__ int ragged_slices(int n, int d, int elem_bytes, size_t unit_bytes) {
+  const int w = ragged_slice_width(n, d, elem_bytes, unit_bytes);
+  return (d + w - 1) / w;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kRaggedThreads) void pool_ragged_kernel(
+    const T* __restrict__ X, const float* __restrict__ S, const float* __restrict__ H, const int* __restrict__ cu,
+    int B, int d, size_t unit_bytes, float a1, float a2, const float4* __restrict__ coef,
+    float* __restrict__ pooled, float* __restrict__ e, int* __restrict__ top) {
+  __shared__ float wts[kPromptMaxRows];
+  __shared__ __attribute__((aligned(16))) float red[kRaggedThreads * 8];
+  __shared__ int scan[kRaggedThreads / 64];
+  __shared__ int unit[2];
+  __shared__ float shv[kRaggedThreads / 64];
+  __shared__ int shi[kRaggedThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // ---- which (prompt, slice) is unit blockIdx.x: scan of the per-prompt slice counts
+  {
+    const int per = (B + kRaggedThreads - 1) / kRaggedThreads;  // <= 16
+    const int b0 = min(B, tid * per), b1 = min(B, b0 + per);
+    int cnt = 0;
+    for (int b = b0; b < b1; ++b) cnt += ragged_slices(cu[b + 1] - cu[b], d, int(sizeof(T)), unit_bytes);
+    int x = cnt;  // inclusive scan within the wave, then over the wave totals
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) scan[wave] = x;
+    if (tid == 0) unit[0] = -1;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += scan[w];
+    const int k = int(blockIdx.x);
+    int first = before + x - cnt;  // this thread's first unit
+    if (k >= first && k < first + cnt) {
+      for (int b = b0; b < b1; ++b) {
+        const int ns = ragged_slices(cu[b + 1] - cu[b], d, int(sizeof(T)), unit_bytes);
+        if (k < first + ns) {
+          unit[0] = b;
+          unit[1] = k - first;
+          break;
+        }
+        first += ns;
+      }
+    }
+    __syncthreads();
+  }
+  const int b = unit[0];
+  if (b < 0) return;  // past the last unit
+  const int slice = unit[1];
+  const int base = cu[b];
+  const int N = min(cu[b + 1] - base, kPromptMaxRows);  // the host guarantees N <= kPromptMaxRows
+  const int F = ragged_slice_width(N, d, int(sizeof(T)), unit_bytes);
+  const int f0 = slice * F;
+  const int G = F / 8;                             // lanes per row
+  const int RP = kRaggedThreads / G;              // row groups (F <= 512 x 8: RP >= 1)
+  const int col = tid % G, rgrp = tid / G;         // this thread's 8 features and first row
+  const int c = f0 + col * 8;
+  const bool active = rgrp < RP && c < d;
+  const T* xp = X + size_t(base) * d + (active ? c : 0);
+  const int nr = active && N > rgrp ? (N - rgrp + RP - 1) / RP : 0;  // rows of this thread: rgrp + RP q
+
+  constexpr int kInFlight = 8;
+  typename Row8<T>::Raw v[kInFlight];
+  const int n_first = min(nr, kInFlight);
+#pragma unroll
+  for (int q = 0; q < kInFlight; ++q)
+    if (q < n_first) v[q] = Row8<T>::load(xp + size_t(rgrp + RP * q) * d);
+
+  // ---- the prompt's weights: u into LDS, first arg-max, exp-sum
+  const float4 cf = coef_of(coef, b, a1, a2);
+  float m = -INFINITY;
+  int mi = 0x7fffffff;
+  for (int i = tid; i < N; i += kRaggedThreads) {
+    const float u = fused_score(cf, S[base + i], H[base + i]);
+    wts[i] = u;
+    if (u > m) {  // increasing i: strict keeps the first
+      m = u;
+      mi = i;
+    }
+  }
+  block_argmax(m, mi, shv, shi);
+  float z = 0.f;
+  for (int i = tid; i < N; i += kRaggedThreads) {
+    const float p = fast_exp2((wts[i] - m) * kLog2e);
+    wts[i] = p;
+    z += p;
+  }
+  z = block_sum(z, shv);  // its barriers also publish wts
+  const float invZ = 1.f / z;
+  if (slice == 0) {
+    if (e)
+      for (int i = tid; i < N; i += kRaggedThreads) e[base + i] = wts[i] * invZ;
+    if (top && tid == 0) top[b] = base + mi;
+  }
+
+  // ---- stream the slice: 8 rows in flight per thread
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const float* w = wts + rgrp;  // weight of this thread's q-th row: w[RP * q]
+#pragma unroll
+  for (int q = 0; q < kInFlight; ++q)
+    if (q < n_first) Row8<T>::fma8(w[RP * q], v[q], acc);
+  int q = n_first;
+  for (; q + kInFlight <= nr; q += kInFlight) {
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k) v[k] = Row8<T>::load(xp + size_t(rgrp + RP * (q + k)) * d);
+#pragma unroll
+    for (int k = 0; k < kInFlight; ++k) Row8<T>::fma8(w[RP * (q + k)], v[k], acc);
+  }
+  for (; q < nr; ++q) Row8<T>::fma8(w[RP * q], Row8<T>::load(xp + size_t(rgrp + RP * q) * d), acc);
+
+  // ---- add the RP row groups of each feature in a fixed order
+  float* rw = red + tid * 8;
+  *reinterpret_cast<float4*>(rw) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  *reinterpret_cast<float4*>(rw + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  __syncthreads();
+  for (int f = tid; f < F; f += kRaggedThreads) {
+    if (f0 + f >= d) break;
+    float sum = 0.f;
+    for (int g = 0; g < RP; ++g) sum += red[(g * G + f / 8) * 8 + f % 8];
+    pooled[size_t(b) * d + f0 + f] = sum * invZ;
   }
 }
 
@@ -479,7 +674,7 @@ __global__ __launch_bounds__(kThreads) void pool_finish_kernel(const float* __re
   if (weights) {
     if (wi < N) {
       const float4 cf = coef_of(coef, b, a1, a2);
-      const float u = fmaf(cf.x, sv, fmaf(cf.y, hv, cf.z));
+      const float u = fused_score(cf, sv, hv);
       e[base + wi] = fast_exp2((u - M) * kLog2e) * invZ;
     }
     return;
@@ -534,6 +729,28 @@ bool use_prompt_path(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t d) {
   if (n_cu < 1) return false;
   const size_t wg = size_t(B) * ((size_t(d) + kPromptSlice - 1) / kPromptSlice);
   return wg >= size_t(n_cu) && (wg % size_t(n_cu) == 0 || wg >= 4 * size_t(n_cu));
+}
+// Prompts no longer than the LDS weight buffer, and few enough for the in-kernel scan: one kernel
+// with length-sized feature slices (pool_ragged_kernel) instead of chunk partials and a finisher.
+bool use_ragged_path(int32_t B, int32_t max_seqlen) {
+  return max_seqlen <= kPromptMaxRows && B <= kRaggedMaxPrompts;
+}
+
+// X bytes per unit: about four units per compute unit over the batch, within [64 KB, 512 KB].
+size_t ragged_unit_bytes(int64_t n_tok, int32_t d, size_t esz) {
+  const int n_cu = std::max(1, current_device_cu_count());
+  const size_t total = size_t(n_tok) * size_t(d) * esz;
+  return std::min(kRaggedMaxUnitBytes, std::max(kRaggedMinUnitBytes, total / (4 * size_t(n_cu))));
+}
+
+// Upper bound on sum_b ragged_slices(N_b): a prompt of bytes_b takes at most
+// max(min slices, bytes_b / unit) slices (the nonempty ones of that width are no more), so the sum
+// is at most total / unit + B * min slices; never more than d / kRaggedMinSlice (or the minimum)
+// per prompt.
+size_t ragged_unit_bound(int64_t n_tok, int32_t B, int32_t d, size_t esz, size_t unit) {
+  const size_t per_max = std::max<size_t>(size_t(ragged_min_slices(d)), size_t(d) / kRaggedMinSlice);
+  const size_t bound = size_t(n_tok) * size_t(d) * esz / unit + size_t(B) * size_t(ragged_min_slices(d));
+  return std::min(bound, size_t(B) * per_max);
 }
 }  // namespace
 
@@ -625,6 +842,22 @@ extern "C" int estp_combine_pool(const void* X, const float* S, const float* H, 
                                                                        int(d), ns, a1, a2, cf, pooled, e, top);
     }
     ESTP_CHECK_LAUNCH("pool_prompt_kernel");
+    return ESTP_OK;
+  }
+  if (use_ragged_path(B, max_seqlen)) {
+    const size_t esz = dtype == ESTP_BF16 ? 2 : 4;
+    const size_t ub = ragged_unit_bytes(n_tok, d, esz);
+    const size_t n_units = ragged_unit_bound(n_tok, B, d, esz, ub);
+    ESTP_REQUIRE(fits_launch(n_units, kRaggedThreads), ESTP_ERR_UNSUPPORTED,
+                 "estp_combine_pool: batch too large for one launch");
+    if (dtype == ESTP_BF16) {
+      pool_ragged_kernel<uint16_t><<<dim3(unsigned(n_units)), dim3(kRaggedThreads), 0, s>>>(
+          static_cast<const uint16_t*>(X), S, H, cu_seqlens, B, int(d), ub, a1, a2, cf, pooled, e, top);
+    } else {
+      pool_ragged_kernel<float><<<dim3(unsigned(n_units)), dim3(kRaggedThreads), 0, s>>>(
+          static_cast<const float*>(X), S, H, cu_seqlens, B, int(d), ub, a1, a2, cf, pooled, e, top);
+    }
+    ESTP_CHECK_LAUNCH("pool_ragged_kernel");
     return ESTP_OK;
   }
   if (use_map) {

@@ -23,14 +23,16 @@ pytestmark = pytest.mark.gpu
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
-LENGTHS = [1000, 10, 5, 300, 2, 700, 1, 40, 257, 256, 3, 999] * 3
+# one prompt over 8192 tokens sends the pooling through its list of live chunks
+LENGTHS = [9000] + [1000, 10, 5, 300, 2, 700, 1, 40, 257, 256, 3, 999] * 3
+MAX_LEN = max(LENGTHS)
 
 CHILD = r"""
 import sys, numpy as np, torch
 sys.path.insert(0, ROOT)
 import paper_2608_15592_amd as estp
 from paper_2608_15592_amd import _lib
-from tests.test_gpu_debug_checks import make_inputs, run_calls
+from tests.test_gpu_debug_checks import MAX_LEN, make_inputs, run_calls
 lib = estp.load()
 if lib.estp_debug_checks() != 1:
     print("debug checks are off"); sys.exit(3)
@@ -51,9 +53,9 @@ for name, cu in bad.items():
     for call in ("importance", "pool", "misalignment"):
         try:
             if call == "importance":
-                estp.attn_importance(Q, K, cud, 1000)
+                estp.attn_importance(Q, K, cud, MAX_LEN)
             elif call == "pool":
-                estp.combine_pool(X, S, H, cud, 1000, 0.5, 0.5)
+                estp.combine_pool(X, S, H, cud, MAX_LEN, 0.5, 0.5)
             else:
                 if name == "last offset past n_tok":
                     continue  # the call does not state n_tok
@@ -65,7 +67,7 @@ for name, cu in bad.items():
         print(f"NOT refused: {call}, {name}"); sys.exit(4)
 # a prompt longer than the stated max_seqlen
 try:
-    estp.attn_importance(Q, K, inp["cu"], 999)
+    estp.attn_importance(Q, K, inp["cu"], MAX_LEN - 1)
     print("NOT refused: max_seqlen"); sys.exit(4)
 except estp.EstpError as e:
     assert e.status == 1 and "debug check" in str(e)
@@ -87,8 +89,8 @@ def make_inputs():
 
 
 def run_calls(inp):
-    S = estp.attn_importance(inp["Q"], inp["K"], inp["cu"], max(LENGTHS))
-    pooled, e, top = estp.combine_pool(inp["X"], inp["S"], inp["H"], inp["cu"], max(LENGTHS), 0.5, 0.5, 1.0, "zscore")
+    S = estp.attn_importance(inp["Q"], inp["K"], inp["cu"], MAX_LEN)
+    pooled, e, top = estp.combine_pool(inp["X"], inp["S"], inp["H"], inp["cu"], MAX_LEN, 0.5, 0.5, 1.0, "zscore")
     counts = estp.misalignment(inp["H"], inp["S"], inp["cu"])
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in (("S", S), ("pooled", pooled), ("e", e), ("top", top), ("counts", counts))}

@@ -364,6 +364,54 @@ def test_combine_pool_many_short_prompts():
         check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
 
 
+POOL_PATH_CASES = [
+    # (lengths, d, dtype, tag): which pooling kernel a batch takes follows from its shape
+    ("mixed-1-3000", 8200, "bf16", "one-kernel, width 8200: four minimum slices"),
+    ("many-1-20", 128, "bf16", "one-kernel, 3000 prompts in the in-kernel scan"),
+    ("mixed-1-3000", 1000, "f32", "one-kernel, fp32 hidden states"),
+    ([9000, 5, 300], 264, "bf16", "chunked (prompt over 8192 rows), list of live chunks"),
+    ([8500, 8400], 136, "f32", "chunked, full prompt x chunk grid"),
+    ("many-1-3", 64, "bf16", "chunked (over 8192 prompts), list of live chunks"),
+]
+
+
+def _pool_lengths(spec, g):
+    if spec == "mixed-1-3000":
+        return [3000, 1, 2] + np.exp(g.uniform(0, np.log(3000), size=21)).astype(int).tolist()
+    if spec == "many-1-20":
+        return g.integers(1, 21, size=3000).tolist()
+    if spec == "many-1-3":
+        return g.integers(1, 4, size=9000).tolist()
+    return list(spec)
+
+
+@pytest.mark.parametrize("spec,d,xdtype,tag", POOL_PATH_CASES, ids=[c[-1] for c in POOL_PATH_CASES])
+def test_combine_pool_paths(spec, d, xdtype, tag):
+    g = np.random.default_rng(len(tag) + d)
+    lengths = _pool_lengths(spec, g)
+    n = sum(lengths)
+    Xf = g.standard_normal((n, d)).astype(np.float32)
+    X = _bf16(Xf) if xdtype == "bf16" else Xf
+    S = (g.random(n) / 20).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    Xd, Sd, Hd, cud = dev(X), dev(S), dev(Hh), dev(cu)
+    for l1, l2, a, norm in [(0.5, 0.5, 1.0, "none"), (0.8, 0.2, 0.5, "zscore")]:
+        pooled, e, top = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
+        e_ref, _ = oracle.combine_weights(S, Hh, cu, l1, l2, a, norm)
+        p_ref = oracle.pool(X, e_ref, cu)
+        np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+        P, top = host(pooled), host(top)
+        errs = [rel_l2(P[b], p_ref[b]) for b in range(len(lengths))]
+        print(f"{tag}: {len(lengths)} prompts, max pooled rel L2 {max(errs):.1e}")
+        assert max(errs) <= POOL_RTOL
+        for b in range(len(lengths)):
+            lo, hi = cu[b], cu[b + 1]
+            check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
+        again, _, _ = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
+        assert torch.equal(again, pooled)
+
+
 # ------------------------------------------------------------------------------------------ length head
 
 @pytest.mark.parametrize("K,act,B,d,Hdn", [(1, "relu", 37, 256, 96), (8, "relu", 37, 256, 96),
