@@ -2,7 +2,9 @@
 
 Python face of libestp.so: the four calls of the ESTP path (arXiv 2608.15592)
 
-* ``token_entropy``   - Eq. 2, fused LM-head GEMM with streaming entropy
+* ``token_entropy``   - Eq. 2, fused LM-head GEMM with streaming entropy (and, optionally,
+  each token's most probable next token); ``token_entropy_noalloc`` - the same with the
+  library's own scratch, allocating nothing
 * ``attn_importance`` - Eq. 1, two-pass causal attention column means
 * ``attn_importance_from_lse`` - Eq. 1 from a prefill's per-row log-sum-exps (one pass)
 * ``attn_importance_ex`` - Eq. 1 variants: diagonal left out, per-layer weights, optional LSEs
@@ -29,6 +31,7 @@ from ._lib import (  # noqa: F401
     misalignment,
     sjf_padding,
     token_entropy,
+    token_entropy_noalloc,
     token_entropy_workspace_size,
 )
 from .path import run_path  # noqa: F401

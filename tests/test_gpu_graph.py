@@ -64,3 +64,38 @@ def test_path_replays_in_a_hip_graph(workload, overrides):
         torch.cuda.synchronize()
         for k, ref in eager.items():
             assert torch.equal(outs[k], ref), f"replay {rep}: {k} differs from the eager step"
+
+
+def test_noalloc_entropy_replays_in_a_hip_graph():
+    # estp_token_entropy_noalloc is for callers that cannot allocate, such as code under graph
+    # capture: captured once with no workspace, replayed after eager calls that overwrite its
+    # scratch with another problem's partial states; each replay equals the workspace entry point
+    g = np.random.default_rng(5)
+    n, d, V = 3000, 512, 30000
+    X = dev(I.f32_to_bf16_bits((g.standard_normal((n, d)) / 1.0).astype(np.float32)))
+    W = dev(I.f32_to_bf16_bits((g.standard_normal((V, d)) * 0.02).astype(np.float32)))
+    X2 = dev(I.f32_to_bf16_bits(g.standard_normal((700, d)).astype(np.float32)))
+    am_ref = torch.empty(n, dtype=torch.int32, device="cuda")
+    H_ref = estp.token_entropy(X, W, vocab_argmax=am_ref)
+    H = torch.empty(n, device="cuda")
+    am = torch.empty(n, dtype=torch.int32, device="cuda")
+    H2 = torch.empty(700, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        estp.token_entropy_noalloc(X, W, H, vocab_argmax=am)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        estp.token_entropy_noalloc(X, W, H, vocab_argmax=am)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        H.fill_(float("nan"))
+        am.fill_(-1)
+        estp.token_entropy_noalloc(X2, W, H2)  # eager call on the same scratch, another problem
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(H, H_ref), f"replay {rep}: H"
+        assert torch.equal(am, am_ref), f"replay {rep}: argmax"
