@@ -59,6 +59,19 @@ inline size_t block_rows(int64_t n_tok, int32_t B, int32_t max_seqlen) {
   return use_block_list(n_tok, B, max_seqlen) ? block_bound(n_tok, B, max_seqlen) : size_t(B) * nqb;
 }
 
+// Query heads of one KV group are split over `nsplit` pass-2 workgroups when the grid would
+// otherwise be small: the smallest divisor of G = Hq / Hkv that gives at least four workgroups per
+// compute unit (else G, one head each).  The fp32 kernels keep one workgroup per group.
+inline int colsum_split(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L, int32_t Hq, int32_t Hkv, bool f32) {
+  if (f32) return 1;
+  const int G = Hq / Hkv;
+  const int n_cu = std::max(1, current_device_cu_count());
+  const size_t base = block_rows(n_tok, B, max_seqlen) * size_t(L) * size_t(Hkv);
+  for (int d = 1; d < G; ++d)
+    if (G % d == 0 && base * size_t(d) >= size_t(4) * n_cu) return d;
+  return G;
+}
+
 // Rows of DH bf16 staged in LDS: 16-byte chunks XOR-swizzled so that 16
 // consecutive rows read at one logical chunk hit 16 distinct bank groups.
 template <int DH>
@@ -256,7 +269,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
                                                                int L, int Hq, int Hkv, float c2,
                                                                const float* __restrict__ lse2, float lse_mul,
                                                                int strict, const int2* __restrict__ blist,
-                                                               int n_blist, float* __restrict__ part) {
+                                                               int n_blist, int nsplit, float* __restrict__ part) {
   constexpr int KS = DH / 16;
   using T = RowTile<DH>;
   constexpr int kTileBytes = kQTile * T::kRowBytes;
@@ -264,12 +277,14 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   __shared__ __attribute__((aligned(16))) float ltile[2][kQTile];
 
   const int G = Hq / Hkv;
-  // block -> (key block, prompt, layer * Hkv + kv head); key block 0 (the most work) first
-  // or the list of live 256-row blocks walked from its end (lightest first there, so heaviest
-  // first here; the padding entries past the live ones come first and exit at once)
+  const int hpw = G / nsplit;  // query heads this workgroup walks: hs * hpw .. of the group
+  // block -> (key block, prompt, (layer * Hkv + kv head) * nsplit + head share); key block 0 (the
+  // most work) first, or the list of live 256-row blocks walked from its end (lightest first
+  // there, so heaviest first here; the padding entries past the live ones come first and exit)
   int idx = blockIdx.x;
-  const int lg = idx % (L * Hkv);
-  idx /= L * Hkv;
+  const int lgs = idx % (L * Hkv * nsplit);
+  idx /= L * Hkv * nsplit;
+  const int lg = lgs / nsplit, hs = lgs % nsplit;
   int b, kblk;
   if (blist) {
     const int2 e = blist[n_blist - 1 - idx];
@@ -309,16 +324,17 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   // tiles: (query block qb, head) for qb from the block's first key on; head fastest
   const int qb_first = kblk * (kKBlock / kQTile);
   const int n_qb = (N + kQTile - 1) / kQTile - qb_first;
-  const int n_tiles = n_qb * G;
+  const int n_tiles = n_qb * hpw;
+  const int h0 = g * G + hs * hpw;  // first query head of this workgroup's share
   auto stage = [&](int t, int buf) {
-    const int hh = g * G + t % G;
-    const int qb = qb_first + t / G;
+    const int hh = h0 + t % hpw;
+    const int qb = qb_first + t / hpw;
     stage_rows<DH>(qtile[buf], kQTile, wave, 4, lane,
                    [&](int r) { return Ql + size_t(min(qb * kQTile + r, N - 1)) * qrow + size_t(hh) * DH; });
   };
   auto lse_load = [&](int t) {  // lanes below kQTile of wave 0 fetch the tile's row LSEs
-    const int hh = g * G + t % G;
-    const int i = (qb_first + t / G) * kQTile + lane;
+    const int hh = h0 + t % hpw;
+    const int i = (qb_first + t / hpw) * kQTile + lane;
     return (lane < kQTile && i < N) ? Ll[size_t(hh) * n_tok + i] * lse_mul : INFINITY;  // rows past N weigh 0
   };
 
@@ -333,7 +349,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
       stage(t + 1, (t + 1) & 1);
       if (wave == 0) lv = lse_load(t + 1);
     }
-    const int qb = qb_first + t / G;
+    const int qb = qb_first + t / hpw;
     const int i0 = qb * kQTile;
     if (i0 + kQTile - 1 >= k0 && k0 < N) {  // some query of the tile sees some key of this wave
       const char* qt = qtile[t & 1];
@@ -394,7 +410,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   for (int cb = 0; cb < 2; ++cb) {
     csum[cb] += __shfl_xor(csum[cb], 32, 64);
     const int j = k0 + cb * 32 + col;
-    if (half == 0 && j < N) part[(size_t(l) * Hkv + g) * n_tok + base + j] = csum[cb];
+    if (half == 0 && j < N) part[((size_t(l) * Hkv + g) * nsplit + hs) * n_tok + base + j] = csum[cb];
   }
 }
 
@@ -437,7 +453,8 @@ struct LayerWeights {
   float w[kMaxWeightedLayers];
 };
 
-// S_j = (sum over layers l and KV heads of w_l times the column masses) / (N * Hq)
+// S_j = (sum over layers l and the column-mass rows of each layer (KV heads, or shares of their
+// query heads) of w_l times the column masses) / (N * Hq); `Hkv` here counts those rows per layer
 __global__ __launch_bounds__(256) void attn_reduce_kernel(const float* __restrict__ part, const int* __restrict__ cu,
                                                           int n_tok, int L, int Hkv, int Hq, int weighted,
                                                           LayerWeights lw, float* __restrict__ S) {
@@ -471,6 +488,7 @@ template <int DH>
 int launch(const char* fn, const void* Qv, const void* Kv, bool f32, const int* cu, int B, int max_seqlen, int n_tok,
            int L, int Hq, int Hkv, float scale, const float* lse_in, int strict, const float* layer_weights, float* S,
            float* lse2, float* part, int2* blist, hipStream_t s) {
+  const int nsplit = colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, f32);  // part holds L * Hkv * nsplit rows
   static_assert(kQBlock == kKBlock, "the two passes share one list of 256-row blocks");
   const float c2 = scale * kLog2e;
   const int nqb = (max_seqlen + kQBlock - 1) / kQBlock;
@@ -509,14 +527,13 @@ int launch(const char* fn, const void* Qv, const void* Kv, bool f32, const int* 
     if (!lse_in)
       attn_lse_kernel<DH><<<dim3(n_wg), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, nqb, c2, bl,
                                                                  xcd_groups, lse2);
-    attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv), dim3(kThreads), 0, s>>>(Q, K, cu, B, n_tok, L, Hq, Hkv, c2,
-                                                                              lse2, lse_mul, strict, bl, int(n_bound),
-                                                                              part);
+    attn_colsum_kernel<DH><<<dim3(n_rows * L * Hkv * nsplit), dim3(kThreads), 0, s>>>(
+        Q, K, cu, B, n_tok, L, Hq, Hkv, c2, lse2, lse_mul, strict, bl, int(n_bound), nsplit, part);
   }
   LayerWeights lw{};
   if (layer_weights)
     for (int l = 0; l < L; ++l) lw.w[l] = layer_weights[l];
-  attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L, Hkv, Hq,
+  attn_reduce_kernel<<<dim3((max_seqlen + 255) / 256, B), dim3(256), 0, s>>>(part, cu, n_tok, L, Hkv * nsplit, Hq,
                                                                              layer_weights ? 1 : 0, lw, S);
   ESTP_CHECK_LAUNCH(fn);
   return ESTP_OK;
@@ -574,14 +591,12 @@ int launch_dh(const char* fn, int dh, const void* q, const void* k, bool f32, co
 
 extern "C" size_t estp_attn_importance_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen, int32_t L,
                                                       int32_t Hq, int32_t Hkv, int32_t dh, int dtype) {
-  (void)B;
-  (void)max_seqlen;
   (void)dh;
-  (void)dtype;
-  if (n_tok < 1 || L < 1 || Hq < 1 || Hkv < 1) return 0;
+  if (n_tok < 1 || B < 1 || max_seqlen < 1 || L < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return 0;
   Carver c(nullptr);
   c.take<float>(size_t(L) * Hq * n_tok);   // lse2 [L, Hq, n_tok]
-  c.take<float>(size_t(L) * Hkv * n_tok);  // column masses [L, Hkv, n_tok]
+  c.take<float>(size_t(L) * Hkv * colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, dtype == ESTP_F32) *
+                n_tok);  // column masses [L, Hkv * nsplit, n_tok]
   c.take<int2>(block_bound(n_tok, B, max_seqlen));  // list of live 256-row blocks
   return c.bytes();
 }
@@ -602,7 +617,8 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
 
   Carver c(workspace);
   float* lse2 = c.take<float>(size_t(L) * Hq * n_tok);
-  float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  float* part = c.take<float>(size_t(L) * Hkv * colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, dtype == ESTP_F32) *
+                              n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   return launch_dh("estp_attn_importance", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen, int(n_tok), L, Hq,
                    Hkv, scale, nullptr, 0, nullptr, S, lse2, part, blist, static_cast<hipStream_t>(stream));
@@ -611,14 +627,11 @@ extern "C" int estp_attn_importance(const void* Q, const void* K, const int32_t*
 extern "C" size_t estp_attn_importance_from_lse_workspace_size(int64_t n_tok, int32_t B, int32_t max_seqlen,
                                                                int32_t L, int32_t Hq, int32_t Hkv, int32_t dh,
                                                                int dtype) {
-  (void)B;
-  (void)max_seqlen;
-  (void)Hq;
   (void)dh;
-  (void)dtype;
-  if (n_tok < 1 || L < 1 || Hkv < 1) return 0;
+  if (n_tok < 1 || B < 1 || max_seqlen < 1 || L < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return 0;
   Carver c(nullptr);
-  c.take<float>(size_t(L) * Hkv * n_tok);  // column masses [L, Hkv, n_tok]
+  c.take<float>(size_t(L) * Hkv * colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, dtype == ESTP_F32) *
+                n_tok);  // column masses [L, Hkv * nsplit, n_tok]
   c.take<int2>(block_bound(n_tok, B, max_seqlen));  // list of live 256-row blocks
   return c.bytes();
 }
@@ -639,7 +652,8 @@ extern "C" int estp_attn_importance_from_lse(const void* Q, const void* K, const
                "estp_attn_importance_from_lse: workspace must be non-null and 256-byte aligned");
 
   Carver c(workspace);
-  float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  float* part = c.take<float>(size_t(L) * Hkv * colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, dtype == ESTP_F32) *
+                              n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   return launch_dh("estp_attn_importance_from_lse", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen,
                    int(n_tok), L, Hq, Hkv, scale, lse, 0, nullptr, S, nullptr, part, blist,
@@ -677,7 +691,8 @@ extern "C" int estp_attn_importance_ex(const void* Q, const void* K, const float
                "estp_attn_importance_ex: workspace must be non-null and 256-byte aligned");
   Carver c(workspace);
   float* lse2 = lse ? nullptr : c.take<float>(size_t(L) * Hq * n_tok);
-  float* part = c.take<float>(size_t(L) * Hkv * n_tok);
+  float* part = c.take<float>(size_t(L) * Hkv * colsum_split(n_tok, B, max_seqlen, L, Hq, Hkv, dtype == ESTP_F32) *
+                              n_tok);
   int2* blist = c.take<int2>(block_bound(n_tok, B, max_seqlen));
   return launch_dh("estp_attn_importance_ex", dh, Q, K, dtype == ESTP_F32, cu_seqlens, B, max_seqlen, int(n_tok), L,
                    Hq, Hkv, scale, lse, (flags & ESTP_IMPORTANCE_EXCLUDE_SELF) ? 1 : 0, layer_weights, S, lse2, part,
