@@ -410,25 +410,24 @@ __global__ __launch_bounds__(kPromptThreads) void pool_prompt_kernel(
 
 // One-kernel pooling of a ragged batch.  Work unit = (prompt, feature slice),
 // like pool_prompt_kernel, but the slice width follows the prompt's length so
-// that every unit streams about kRaggedUnitBytes of X: a short prompt takes
-// whole rows, a 4096-token one 128 of 4096 features.  Each unit sums all rows
-// of its prompt for its slice, so there are no partials and no second kernel.
-// The units of a prompt are consecutive; a workgroup finds its (prompt, slice)
-// by scanning the prompt lengths itself (no list kernel).  G = F / 8 lanes
-// cover one row (16-byte loads), 512 / G rows are in flight per load round and
-// 8 rounds per thread; the row groups' sums are added in a fixed order.
+// that every unit streams about the same number of bytes of X (512 KB, less
+// for small batches: four units per compute unit): a short prompt takes whole
+// rows, a 4096-token one 128 of 4096 features.  Each unit sums all rows of its
+// prompt for its slice, so there are no partials and no second kernel.  The
+// units of a prompt are consecutive; a workgroup finds its (prompt, slice) by
+// scanning the prompt lengths itself (no list kernel).  G = F / 8 lanes cover
+// one row (16-byte loads), 512 / G rows are in flight per load round and 8
+// rounds per thread; the row groups' sums are added in a fixed order.
+// Unit size, slice alignment and the narrowest slice were swept on MI355X over
+// the ragged, Qwen-shaped and 1B-shaped batches: 512 KB units, widths a
+// multiple of 64 features (whole 128-byte lines of bf16), at least 128 features.
 constexpr int kRaggedThreads = 512;
 constexpr int kRaggedMaxPrompts = 8192;  // prompts the in-kernel scan covers (16 per thread)
-constexpr int kRaggedMinSlice = 64;      // narrowest slice: 128-byte bf16 rows
-#ifndef ESTP_RAGGED_MAX_UNIT_BYTES
-#define ESTP_RAGGED_MAX_UNIT_BYTES (size_t(512) << 10)
-#endif
-#ifndef ESTP_RAGGED_ALIGN
-#define ESTP_RAGGED_ALIGN 64
-#endif
-constexpr size_t kRaggedMaxUnitBytes = ESTP_RAGGED_MAX_UNIT_BYTES;
+constexpr int kRaggedMinSlice = 128;     // narrowest slice (features)
+constexpr int kRaggedUnitsPerCu = 4;
+constexpr size_t kRaggedMaxUnitBytes = size_t(512) << 10;
 constexpr size_t kRaggedMinUnitBytes = size_t(64) << 10;
-constexpr int kRaggedAlign = ESTP_RAGGED_ALIGN;  // slice widths are multiples of this many features
+constexpr int kRaggedAlign = 64;         // slice widths are multiples of this many features
 
 // Width of one of ns slices of d features, a multiple of kRaggedAlign (at least the 8 of a
 // 16-byte bf16 load), and never more than the workgroup covers.
@@ -740,7 +739,7 @@ bool use_ragged_path(int32_t B, int32_t max_seqlen) {
 size_t ragged_unit_bytes(int64_t n_tok, int32_t d, size_t esz) {
   const int n_cu = std::max(1, current_device_cu_count());
   const size_t total = size_t(n_tok) * size_t(d) * esz;
-  return std::min(kRaggedMaxUnitBytes, std::max(kRaggedMinUnitBytes, total / (4 * size_t(n_cu))));
+  return std::min(kRaggedMaxUnitBytes, std::max(kRaggedMinUnitBytes, total / (size_t(kRaggedUnitsPerCu) * size_t(n_cu))));
 }
 
 // Upper bound on sum_b ragged_slices(N_b): a prompt of bytes_b takes at most
