@@ -358,6 +358,25 @@ def main() -> int:
         del g
         log(f"graph replay: {gms:.3f} ms/step (eager {ms_per_step:.3f})")
 
+    # The entropy call that also returns each token's most probable next token, timed on its own
+    # against the plain call, interleaved (median of 3 each); its output goes to buffers of its own.
+    am = torch.empty(n_tok, dtype=torch.int32, device=X.device)
+    H_am = torch.empty(n_tok, dtype=torch.float32, device=X.device)
+    estp.token_entropy(X, W, H=H_am, vocab_argmax=am, workspace=bufs["ws_entropy"], stream=stream)
+    am_evs = [HipEvent() for _ in range(12)]
+    for k in range(3):
+        am_evs[4 * k].record(stream)
+        estp.token_entropy(X, W, H=H_am, workspace=bufs["ws_entropy"], stream=stream)
+        am_evs[4 * k + 1].record(stream)
+        am_evs[4 * k + 2].record(stream)
+        estp.token_entropy(X, W, H=H_am, vocab_argmax=am, workspace=bufs["ws_entropy"], stream=stream)
+        am_evs[4 * k + 3].record(stream)
+    torch.cuda.synchronize()
+    plain_ms = float(np.median([am_evs[4 * k].elapsed_time(am_evs[4 * k + 1]) for k in range(3)]))
+    am_ms = float(np.median([am_evs[4 * k + 2].elapsed_time(am_evs[4 * k + 3]) for k in range(3)]))
+    del am, H_am
+    log(f"entropy with next-token mode: {am_ms:.3f} ms (plain {plain_ms:.3f} ms)")
+
     # The one-pass importance call fed with a prefill's row log-sum-exps (here formed with plain
     # fp32 torch, untimed); timed on its own, outside the step.
     lse = row_lse_torch(Q, K, inp["cu_seqlens"], w.dh ** -0.5, torch)
@@ -522,6 +541,9 @@ def main() -> int:
                        "exp_roofline": {"bound": "alu", "exps": imp_exps, "achieved": imp_exps / (imp_ms * 1e-3),
                                         "peak": PEAK_EXP_PER_S, "unit": "exp/s",
                                         "frac": imp_exps / (imp_ms * 1e-3) / PEAK_EXP_PER_S}},
+        "entropy_with_vocab_argmax": {"ms": am_ms, "plain_ms": plain_ms, "overhead": am_ms / plain_ms - 1.0,
+                                      "note": "estp_token_entropy with the vocab_argmax output against the plain "
+                                              "call, interleaved, median of 3 each; not part of the timed step"},
         "importance_from_prefill_lse": {"ms": lse_ms, "vs_two_pass": lse_ms / imp_ms,
                                         "note": "estp_attn_importance_from_lse with given row LSEs; not part of "
                                                 "the timed step"},
