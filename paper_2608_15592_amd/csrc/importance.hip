@@ -30,11 +30,17 @@
 namespace estp {
 namespace detail {
 
-constexpr int kThreads = 256;
-constexpr int kQPerWave = 64;  // queries per wave in pass 1
-constexpr int kQBlock = 4 * kQPerWave;
-constexpr int kKPerWave = 64;  // keys per wave in pass 2
-constexpr int kKBlock = 4 * kKPerWave;
+// 32-wide column blocks a wave keeps resident.  One block per wave (eight waves of 32 rows, four
+// waves per SIMD) was measured slower on MI355X than two: 5.80 against 5.50 ms per call on 32 x
+// 2048 tokens, 32/8 heads of 128, 4 layers (twice the LDS fragment reads per MFMA).
+constexpr int kNC = 2;
+constexpr int kWaves = 8 / kNC;       // waves per 256-row block
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMinBlocks = 3;         // workgroups per CU the register budget is sized for
+constexpr int kQPerWave = 32 * kNC;  // queries per wave in pass 1
+constexpr int kQBlock = kWaves * kQPerWave;
+constexpr int kKPerWave = 32 * kNC;  // keys per wave in pass 2
+constexpr int kKBlock = kWaves * kKPerWave;
 constexpr int kKTile = 64;     // keys per streamed tile in pass 1
 constexpr int kQTile = 64;     // queries per streamed tile in pass 2 (two 32-query row blocks in turn)
 static_assert(kKBlock % kQTile == 0 && kQTile % 32 == 0, "pass-2 tiles must tile a key block");
@@ -101,7 +107,7 @@ __device__ __forceinline__ void stage_rows(char* dst, int rows, int wave, int nw
 
 // ---------------------------------------------------------------- pass 1
 template <int DH>
-__global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* __restrict__ Q,
+__global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const uint16_t* __restrict__ Q,
                                                             const uint16_t* __restrict__ K,
                                                             const int* __restrict__ cu, int B, int n_tok,
                                                             int L, int Hq, int Hkv, int nqb_max, float c2,
@@ -160,18 +166,23 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
   const int n_kt = (q_hi - 1) / kKTile + 1;           // key tiles the block needs
 
   // queries as B fragments: column cb*32 + col, k = 16 ks + 8 half
-  bf16x8_t bq[2][KS];
+  bf16x8_t bq[kNC][KS];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kNC; ++cb) {
     const int qi = min(q0 + cb * 32 + col, N - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       bq[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Qh + size_t(qi) * qrow + ks * 16 + half * 8);
   }
-  float m[2] = {-INFINITY, -INFINITY}, s[2] = {0.f, 0.f};
+  float m[kNC], s[kNC];
+#pragma unroll
+  for (int cb = 0; cb < kNC; ++cb) {
+    m[cb] = -INFINITY;
+    s[cb] = 0.f;
+  }
 
   auto stage = [&](int kt, int buf) {
-    stage_rows<DH>(ktile[buf], kKTile, wave, 4, lane,
+    stage_rows<DH>(ktile[buf], kKTile, wave, kWaves, lane,
                    [&](int r) { return Kg + size_t(min(kt * kKTile + r, N - 1)) * krow; });
   };
   stage(0, 0);
@@ -182,11 +193,11 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
     const int k0 = kt * kKTile;
     if (k0 > q0 + kQPerWave - 1 || q0 >= N) continue;  // whole tile after this wave's queries
     const char* kb = ktile[kt & 1];
-    f32x16_t acc[2][2];
+    f32x16_t acc[2][kNC];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
+      for (int cb = 0; cb < kNC; ++cb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
 #pragma unroll
@@ -195,7 +206,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
       for (int rb = 0; rb < 2; ++rb) {
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + T::off(rb * 32 + col, ks * 2 + half));
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < kNC; ++cb)
           acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[cb][ks], acc[rb][cb], 0, 0, 0);
       }
     }
@@ -207,7 +218,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
     // 2^64 (or a lane with no reference yet) is refolded exactly with its max.
     const bool diag = k0 + kKTile - 1 > q0;
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < kNC; ++cb) {
       if (diag) {
         // key k0 + rb*32 + 4*half + off(r) lies after query qi iff off(r) > qi - k0 - rb*32 - 4*half,
         // with off(r) = 8*(r/4) + r%4 a constant: one compare per score, no index arithmetic
@@ -251,7 +262,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
   }
   // lanes col and col + 32 hold the two row quads of the same query column
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kNC; ++cb) {
     const float mo = __shfl_xor(m[cb], 32, 64);
     const float so = __shfl_xor(s[cb], 32, 64);
     const float M = fmaxf(m[cb], mo);
@@ -263,7 +274,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_lse_kernel(const uint16_t* _
 
 // ---------------------------------------------------------------- pass 2
 template <int DH>
-__global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t* __restrict__ Q,
+__global__ __launch_bounds__(kThreads, kMinBlocks) void attn_colsum_kernel(const uint16_t* __restrict__ Q,
                                                                const uint16_t* __restrict__ K,
                                                                const int* __restrict__ cu, int B, int n_tok,
                                                                int L, int Hq, int Hkv, float c2,
@@ -311,15 +322,17 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
 
   const int k0 = kblk * kKBlock + wave * kKPerWave;  // this wave's first key
   // keys as B fragments, resident for the whole walk
-  bf16x8_t bk[2][KS];
+  bf16x8_t bk[kNC][KS];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kNC; ++cb) {
     const int kj = min(k0 + cb * 32 + col, N - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       bk[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Kg + size_t(kj) * krow + ks * 16 + half * 8);
   }
-  float csum[2] = {0.f, 0.f};
+  float csum[kNC];
+#pragma unroll
+  for (int cb = 0; cb < kNC; ++cb) csum[cb] = 0.f;
 
   // tiles: (query block qb, head) for qb from the block's first key on; head fastest
   const int qb_first = kblk * (kKBlock / kQTile);
@@ -329,7 +342,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   auto stage = [&](int t, int buf) {
     const int hh = h0 + t % hpw;
     const int qb = qb_first + t / hpw;
-    stage_rows<DH>(qtile[buf], kQTile, wave, 4, lane,
+    stage_rows<DH>(qtile[buf], kQTile, wave, kWaves, lane,
                    [&](int r) { return Ql + size_t(min(qb * kQTile + r, N - 1)) * qrow + size_t(hh) * DH; });
   };
   auto lse_load = [&](int t) {  // lanes below kQTile of wave 0 fetch the tile's row LSEs
@@ -361,16 +374,16 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
       // 32 x 64 block of scores without a second set of registers.
 #pragma unroll
       for (int rb = 0; rb < kQTile / 32; ++rb) {
-        f32x16_t acc[2];
+        f32x16_t acc[kNC];
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < kNC; ++cb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(qt + T::off(rb * 32 + col, ks * 2 + half));
 #pragma unroll
-          for (int cb = 0; cb < 2; ++cb)
+          for (int cb = 0; cb < kNC; ++cb)
             acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bk[cb][ks], acc[cb], 0, 0, 0);
         }
         // acc[cb][r]: query i0 + rb*32 + 8*(r/4) + 4*half + r%4, key k0 + cb*32 + col
@@ -384,7 +397,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
           lr[4 * q4 + 3] = v.w;
         }
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
+        for (int cb = 0; cb < kNC; ++cb) {
           float cs = 0.f;
           if (diag) {
             // query i = i0 + rb*32 + 4*half + off(r) counts for key j iff j < i + 1 - strict, i.e.
@@ -407,7 +420,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_colsum_kernel(const uint16_t
   }
   // the two row quads (lane, lane + 32) of each key column
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kNC; ++cb) {
     csum[cb] += __shfl_xor(csum[cb], 32, 64);
     const int j = k0 + cb * 32 + col;
     if (half == 0 && j < N) part[((size_t(l) * Hkv + g) * nsplit + hs) * n_tok + base + j] = csum[cb];
