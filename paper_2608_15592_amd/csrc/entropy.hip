@@ -91,7 +91,7 @@ __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, 
 // Largest logit with its vocabulary index: b wins over a when it is larger, or
 // equal with a lower index (ties go to the lowest index).
 __device__ __forceinline__ void arg_merge(float& av, int& ai, float bv, int bi) {
-  const bool take = bv > av || (bv == av && bi < ai);
+  const bool take = (bv > av) | ((bv == av) & (bi < ai));  // no short circuit: no branches
   av = take ? bv : av;
   ai = take ? bi : ai;
 }
@@ -397,31 +397,6 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
           }
         e = Ent2{mnew, s, t};
       }
-      if (kArg) {
-        // the tile's largest live logit in this column and its row.  The lane's rows are visited
-        // in ascending order, so a strict compare keeps the lowest index among equal logits.
-        // (One separate pass after the fold: a compare inside the fold's two paths overflows the
-        // registers.)
-        float tb = -INFINITY;
-        int ti = 0;
-#pragma unroll
-        for (int i = 0; i < kNB; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool up = (!ragged || i * 16 + r < lim) && acc[i][j][r] > tb;
-            tb = up ? acc[i][j][r] : tb;
-            ti = up ? i * 16 + r : ti;
-          }
-        // the column's candidate over the four lanes that share it, then kept by lane j / 2
-        float cb = tb;
-        int ci = vt * kBV + wv * 128 + 4 * fq + ti;
-#pragma unroll
-        for (int o = 16; o <= 32; o <<= 1) arg_merge(cb, ci, __shfl_xor(cb, o, 64), __shfl_xor(ci, o, 64));
-        if (fq == j / 2 && cb > zmax[j & 1]) {  // strict: an earlier tile keeps equal maxima
-          zmax[j & 1] = cb;
-          zarg[j & 1] = ci;
-        }
-      }
       // rebase to the running log-sum-exp: m += log2 s, s = 1, t = t / s - log2 s
       // (s >= 1 here: the reference never exceeds the largest logit seen, in base 2)
       if (e.s > 0.f) {
@@ -429,6 +404,48 @@ __global__ __launch_bounds__(kWaves * 64, 1) void entropy_gemm_kernel(
         e = Ent2{e.m + dl, 1.f, e.t / e.s - dl};
       }
       st[j] = e;
+    }
+    if (kArg) {
+      // the next-token mode, in a loop of its own so that the eight columns' independent compare
+      // chains interleave.  Per column: the tile's largest live logit, then the lowest of the
+      // lane's rows holding it (rows visited from the last to the first, the last match kept;
+      // ordinals 4 i + r are small constants, no literal moves).  Dead rows of the ragged tile
+      // lie after every live row, so an equal dead row never wins.  No branches inside: every
+      // compare feeds its select.
+      float tb[kNB];
+#pragma unroll
+      for (int j = 0; j < kNB; ++j) tb[j] = -INFINITY;
+      if (ragged) {
+#pragma unroll
+        for (int j = 0; j < kNB; ++j)
+#pragma unroll
+          for (int i = 0; i < kNB; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) tb[j] = fmaxf(tb[j], i * 16 + r < lim ? acc[i][j][r] : -INFINITY);
+      } else {
+#pragma unroll
+        for (int j = 0; j < kNB; ++j)
+#pragma unroll
+          for (int i = 0; i < kNB; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) tb[j] = fmaxf(tb[j], acc[i][j][r]);
+      }
+#pragma unroll
+      for (int j = 0; j < kNB; ++j) {
+        int k = 0;
+#pragma unroll
+        for (int i = kNB - 1; i >= 0; --i)
+#pragma unroll
+          for (int r = 3; r >= 0; --r) k = acc[i][j][r] == tb[j] ? 4 * i + r : k;
+        // the column's candidate over the four lanes that share it, then kept by lane j / 2
+        float cb = tb[j];
+        int ci = vt * kBV + wv * 128 + 4 * fq + (k >> 2) * 16 + (k & 3);
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) arg_merge(cb, ci, __shfl_xor(cb, o, 64), __shfl_xor(ci, o, 64));
+        const bool keep = (fq == j / 2) & (cb > zmax[j & 1]);  // strict: an earlier tile keeps equal maxima
+        zmax[j & 1] = keep ? cb : zmax[j & 1];
+        zarg[j & 1] = keep ? ci : zarg[j & 1];
+      }
     }
   }  // tile
 
