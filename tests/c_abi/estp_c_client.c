@@ -6,7 +6,8 @@
  * memory through the HIP runtime and runs two closed forms through the
  * library, for both input types:
  *   - W = 0 makes every logit 0, so each token's next-token distribution is
- *     uniform and its entropy is ln V (Eq. 2);
+ *     uniform and its entropy is ln V (Eq. 2); all V logits tie, so the mode
+ *     (vocab_argmax) is index 0, the lowest;
  *   - K = 0 makes every score 0, so the causal attention of query i is 1/(i+1)
  *     on keys 0..i and the importance of key j in a prompt of N tokens is
  *     S_j = (H_N - H_j) / N with harmonic numbers H_n = sum_{k=1..n} 1/k (Eq. 1).
@@ -81,9 +82,12 @@ static int entropy_uniform(int dtype) {
   float* h = (float*)malloc((size_t)n * sizeof(float));
   void *X = NULL, *W = NULL, *ws = NULL;
   float* H = NULL;
+  int32_t* A = NULL;
+  int32_t* am = (int32_t*)malloc((size_t)n * sizeof(int32_t));
   size_t wsb, i;
   double err = 0.0;
-  if (!x || !w || !h) return fail("host allocation");
+  int n_bad = 0;
+  if (!x || !w || !h || !am) return fail("host allocation");
   for (i = 0; i < (size_t)n * d; ++i) x[i] = (float)sin(0.37 * (double)i);
   if (upload(&X, x, (size_t)n * d, dtype) || upload(&W, w, (size_t)V * d, dtype)) return 1;
   HIP_OK(hipMalloc((void**)&H, (size_t)n * sizeof(float)));
@@ -94,6 +98,18 @@ static int entropy_uniform(int dtype) {
   HIP_OK(hipMemcpy(h, H, (size_t)n * sizeof(float), hipMemcpyDeviceToHost));
   for (i = 0; i < (size_t)n; ++i) err = fmax(err, fabs((double)h[i] - log((double)V)));
   printf("entropy, uniform logits (%s): max |H - ln V| = %.3g\n", dtype == ESTP_F32 ? "f32" : "bf16", err);
+  /* the same call with the mode: every logit ties, the lowest index wins */
+  HIP_OK(hipMalloc((void**)&A, (size_t)n * sizeof(int32_t)));
+  HIP_OK(hipMemset(A, 0xff, (size_t)n * sizeof(int32_t)));
+  if (estp_token_entropy(X, W, n, d, V, dtype, H, A, ws, wsb, NULL) != ESTP_OK) return fail("estp_token_entropy (mode)");
+  HIP_OK(hipDeviceSynchronize());
+  HIP_OK(hipMemcpy(am, A, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost));
+  for (i = 0; i < (size_t)n; ++i) n_bad += am[i] != 0;
+  printf("next-token mode, all logits tied (%s): %d of %d rows not index 0\n", dtype == ESTP_F32 ? "f32" : "bf16",
+         n_bad, n);
+  HIP_OK(hipFree(A));
+  free(am);
+  if (n_bad) return fail("tied-logit mode");
   HIP_OK(hipFree(X));
   HIP_OK(hipFree(W));
   HIP_OK(hipFree(H));
