@@ -76,15 +76,19 @@ def test_entropy_past_4gib(big):
     assert np.all(Hd >= 0) and np.all(Hd <= np.log(V) + 2e-3)
 
 
-@pytest.mark.parametrize("max_seqlen", [2048, 4096], ids=["one-kernel", "chunked"])
+# The pooling kernel a call takes follows from the batch and the stated max_seqlen: prompts within 12.5%
+# of max_seqlen that fill the chip take the whole-prompt kernel, other batches of prompts up to 8192
+# tokens the length-sized-slice kernel, and a max_seqlen above 8192 the chunked pair.  Prompt 256
+# straddles token 2^19, where X's byte offset passes 2^32.
+@pytest.mark.parametrize("max_seqlen", [2048, 4096, 9000], ids=["whole-prompt-kernel", "ragged-kernel", "chunked"])
 def test_combine_pool_past_4gib(big, max_seqlen):
-    n, cu = big["n"], big["cu"]
+    lengths, cu, n = LENGTHS, big["cu"], big["n"]
     X = _expand(dev(big["xb"]), n)
     pooled, e, top = estp.combine_pool(X, dev(big["S"]), dev(big["H"]), dev(cu), max_seqlen, 0.5, 0.5, 1.0, "none")
     pooled, e, top = host(pooled), host(e), host(top)
     del X
     torch.cuda.empty_cache()
-    B = len(LENGTHS)
+    B = len(lengths)
     for b in (0, 256, B - 1):
         lo, hi = int(cu[b]), int(cu[b + 1])
         cu_b = np.array([0, hi - lo])

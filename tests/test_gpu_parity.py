@@ -372,6 +372,8 @@ POOL_PATH_CASES = [
     ([9000, 5, 300], 264, "bf16", "chunked (prompt over 8192 rows), list of live chunks"),
     ([8500, 8400], 136, "f32", "chunked, full prompt x chunk grid"),
     ("many-1-3", 64, "bf16", "chunked (over 8192 prompts), list of live chunks"),
+    ("n8192-1-4", 72, "bf16", "one-kernel, 8192 prompts: the in-kernel scan's limit"),
+    ("n8193-1-4", 72, "bf16", "chunked, one prompt past the in-kernel scan's limit"),
 ]
 
 
@@ -382,6 +384,8 @@ def _pool_lengths(spec, g):
         return g.integers(1, 21, size=3000).tolist()
     if spec == "many-1-3":
         return g.integers(1, 4, size=9000).tolist()
+    if isinstance(spec, str) and spec.startswith("n") and spec.endswith("-1-4"):
+        return g.integers(1, 5, size=int(spec[1:-4])).tolist()
     return list(spec)
 
 
