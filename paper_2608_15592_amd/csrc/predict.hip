@@ -21,7 +21,6 @@ namespace detail {
 
 constexpr int kTB = 32;     // prompts per tile
 constexpr int kTH = 32;     // hidden units per tile
-constexpr int kTK = 32;     // reduction depth per LDS stage
 constexpr int kKChunk = 256;  // reduction range of one split-K workgroup
 
 __device__ __forceinline__ float act_fn(float x, int act) {
@@ -34,37 +33,74 @@ __device__ __forceinline__ float act_fn(float x, int act) {
 // Split-K partial of the first layer: part[z, b, j] = sum_{k in chunk z} P[b, k] W1[j, k].
 // 256 threads own a 32 x 32 (prompt x hidden) tile, 4 outputs each; the grid spans
 // hidden tiles x prompt tiles x reduction chunks so that W1 is streamed once by
-// hundreds of workgroups even for small batches.
+// hundreds of workgroups even for small batches.  The whole 256-deep chunk of both
+// operands goes into LDS in one round (all loads in flight together, 16 bytes each
+// when rows allow it), stored k-major so that the compute loop reads without bank
+// conflicts; each output is then summed over k in order.
+template <bool kVec>
 __global__ __launch_bounds__(256) void mlp_partial_kernel(const float* __restrict__ P, const float* __restrict__ W1,
                                                           int B, int d, int Hd, float* __restrict__ part) {
-  __shared__ float sp[kTK][kTB + 1];
-  __shared__ float sw[kTK][kTH + 1];
+  __shared__ float sp[kKChunk][kTB + 1];
+  __shared__ float sw[kKChunk][kTH + 1];
   const int th = blockIdx.x * kTH, tb = blockIdx.y * kTB, z = blockIdx.z;
-  const int k_lo = z * kKChunk, k_hi = min(d, k_lo + kKChunk);
+  const int k_lo = z * kKChunk, nk = min(d, k_lo + kKChunk) - k_lo;
   const int tx = threadIdx.x & 31;         // hidden unit in the tile
   const int ty = (threadIdx.x >> 5) * 4;   // first of 4 prompts
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int k0 = k_lo; k0 < k_hi; k0 += kTK) {
-    for (int e = threadIdx.x; e < kTB * kTK; e += 256) {
-      const int r = e / kTK, k = e % kTK;  // consecutive threads read consecutive k of one row
-      const int gk = k0 + k;
-      sp[k][r] = (tb + r < B && gk < k_hi) ? P[size_t(tb + r) * d + gk] : 0.f;
-      sw[k][r] = (th + r < Hd && gk < k_hi) ? W1[size_t(th + r) * d + gk] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int k = 0; k < kTK; ++k) {
-      const float w = sw[k][tx];
+  if (kVec) {
+    // lane (r = lane % 32, h = lane / 32) of wave w loads 16 bytes of row r at depth 4 (2 (w + 4 q) + h)
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 31, h = lane >> 5;
+    float4 vp[8], vw[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] = fmaf(sp[k][ty + i], w, acc[i]);
+    for (int q = 0; q < 8; ++q) {
+      const int k4 = (2 * (wave + 4 * q) + h) * 4;
+      const bool kin = k4 < nk;  // nk is a multiple of 4 here
+      vp[q] = (tb + r < B && kin) ? *reinterpret_cast<const float4*>(P + size_t(tb + r) * d + k_lo + k4)
+                                  : float4{0.f, 0.f, 0.f, 0.f};
+      vw[q] = (th + r < Hd && kin) ? *reinterpret_cast<const float4*>(W1 + size_t(th + r) * d + k_lo + k4)
+                                   : float4{0.f, 0.f, 0.f, 0.f};
     }
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int k4 = (2 * (wave + 4 * q) + h) * 4;
+      sp[k4][r] = vp[q].x;
+      sp[k4 + 1][r] = vp[q].y;
+      sp[k4 + 2][r] = vp[q].z;
+      sp[k4 + 3][r] = vp[q].w;
+      sw[k4][r] = vw[q].x;
+      sw[k4 + 1][r] = vw[q].y;
+      sw[k4 + 2][r] = vw[q].z;
+      sw[k4 + 3][r] = vw[q].w;
+    }
+  } else {
+    for (int e = threadIdx.x; e < kTB * kKChunk; e += 256) {
+      const int r = e / kKChunk, k = e % kKChunk;  // consecutive threads read consecutive k of one row
+      sp[k][r] = (tb + r < B && k < nk) ? P[size_t(tb + r) * d + k_lo + k] : 0.f;
+      sw[k][r] = (th + r < Hd && k < nk) ? W1[size_t(th + r) * d + k_lo + k] : 0.f;
+    }
+  }
+  __syncthreads();
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int k = 0; k < nk; ++k) {
+    const float w = sw[k][tx];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = fmaf(sp[k][ty + i], w, acc[i]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int b = tb + ty + i, j = th + tx;
     if (b < B && j < Hd) part[(size_t(z) * B + b) * Hd + j] = acc[i];
   }
+}
+
+// Launch of the split-K partials: 16-byte loads when every row starts 16-byte aligned.
+void launch_mlp_partial(const float* P, const float* W1, int B, int d, int Hd, float* part, hipStream_t s) {
+  const dim3 grid((Hd + kTH - 1) / kTH, (B + kTB - 1) / kTB, (d + kKChunk - 1) / kKChunk);
+  if (d % 4 == 0 && aligned(P, 16) && aligned(W1, 16))
+    mlp_partial_kernel<true><<<grid, dim3(256), 0, s>>>(P, W1, B, d, Hd, part);
+  else
+    mlp_partial_kernel<false><<<grid, dim3(256), 0, s>>>(P, W1, B, d, Hd, part);
 }
 
 // A[b, j] = act(sum_z part[z, b, j] + b1[j]), chunks summed in order.
@@ -83,7 +119,6 @@ __global__ __launch_bounds__(256) void head_out_kernel(const float* __restrict__
                                                        const float* __restrict__ b2, const float* __restrict__ centres,
                                                        int Hd, int K, float* __restrict__ o_ws,
                                                        float* __restrict__ yhat, int* __restrict__ bin) {
-  __shared__ float red[4];
   const int b = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* a = A + size_t(b) * Hd;
@@ -125,7 +160,6 @@ __global__ __launch_bounds__(256) void head_out_kernel(const float* __restrict__
   }
   z = wave_sum(z);
   zc = wave_sum(zc);
-  (void)red;
   if (lane == 0) {
     yhat[b] = zc / z;
     if (bin) bin[b] = mi;
@@ -366,8 +400,7 @@ extern "C" int estp_predict(const float* pooled, int32_t B, int32_t d, const flo
   float* A = c.take<float>(size_t(B) * hidden);
   float* o = c.take<float>(size_t(B) * K);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  mlp_partial_kernel<<<dim3((hidden + kTH - 1) / kTH, (B + kTB - 1) / kTB, nz), dim3(256), 0, s>>>(pooled, W1, B, d,
-                                                                                                 hidden, part);
+  launch_mlp_partial(pooled, W1, B, d, hidden, part, s);
   ESTP_CHECK_LAUNCH("mlp_partial_kernel");
   mlp_finish_kernel<<<dim3((size_t(B) * hidden + 255) / 256), dim3(256), 0, s>>>(part, b1, B, hidden, nz, act, A);
   ESTP_CHECK_LAUNCH("mlp_finish_kernel");
@@ -449,8 +482,7 @@ extern "C" int estp_head_train_step(const float* pooled, const float* y, int32_t
   opt.bc2 = float(1.0 / (1.0 - std::pow(double(beta2), double(step))));
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t nbh = size_t(B) * hidden;
-  mlp_partial_kernel<<<dim3((hidden + kTH - 1) / kTH, (B + kTB - 1) / kTB, nz), dim3(256), 0, s>>>(pooled, W1, B, d,
-                                                                                                 hidden, part);
+  launch_mlp_partial(pooled, W1, B, d, hidden, part, s);
   ESTP_CHECK_LAUNCH("mlp_partial_kernel");
   train_hidden_kernel<<<dim3((nbh + 255) / 256), dim3(256), 0, s>>>(part, b1, B, hidden, nz, act, Z, A);
   ESTP_CHECK_LAUNCH("train_hidden_kernel");
