@@ -32,13 +32,14 @@
 // kernel that writes H.  When the caller asks for the most probable next
 // token as well, a template variant of the kernel also keeps, per token
 // column, the largest logit and its lowest vocabulary index; the same merges
-// carry it (the variant without it is the plain kernel).  Workgroup ids are
-// remapped so the 32 workgroups
-// resident on one XCD (ids are dealt round-robin over the 8 XCDs) cover 4
-// vocabulary slices x 8 token tiles, and one dispatch wave of 256 covers
-// 16 x 16: concurrent workgroups stream the same W and X tiles through that
-// XCD's L2.  An XCD takes the slices g, g+4, g+8, g+12, so the slices that
-// hold one tile more than the others are spread over the XCDs.
+// carry it (the variant without it is the plain kernel).
+//
+// XCDs.  Workgroup ids are remapped so the 32 workgroups resident on one XCD
+// (ids are dealt round-robin over the 8 XCDs) cover 4 vocabulary slices x 8
+// token tiles, and one dispatch wave of 256 covers 16 x 16: concurrent
+// workgroups stream the same W and X tiles through that XCD's L2.  An XCD
+// takes the slices g, g+4, g+8, g+12, so the slices that hold one tile more
+// than the others are spread over the XCDs.
 #include <atomic>
 #include <mutex>
 

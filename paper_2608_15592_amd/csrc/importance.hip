@@ -14,7 +14,9 @@
 // Pass 2 (attn_colsum_kernel): one workgroup per (layer, KV head, prompt,
 // 256-key block); each wave keeps 64 keys as B fragments in registers and
 // streams, through LDS, every later 64-query block of every query head that
-// shares the KV head (grouped-query reuse: the keys are read once).  Scores
+// shares the KV head (grouped-query reuse: the keys are read once).  When that
+// grid is small, the group's query heads are split over a few workgroups per
+// key block, each writing its own row of column masses.  Scores
 // are formed as S = Q K^T, so a lane owns one key column and 16 query rows of
 // each 32 x 32 block; 2^(c s - lse2) is summed per lane into column sums.
 // Partial column masses per (layer, KV head) are reduced in a fixed order by

@@ -13,7 +13,7 @@
 // asked, the normalised weights e.  With z-scored or min-max scaled inputs a
 // per-prompt statistics pass (zscore_stats_kernel, minmax_stats_kernel) runs
 // first and gives u = c1 (S - centre_S) + c2 (H - centre_H).  Batches of
-// equal-length prompts that fill the chip by themselves take one kernel
+// (nearly) equal-length prompts that fill the chip by themselves take one kernel
 // instead (pool_prompt_kernel: a workgroup streams a whole prompt for one
 // feature slice, so there are no chunk partials to combine), and so do other
 // batches of prompts up to 8192 tokens (pool_ragged_kernel: the slice width
