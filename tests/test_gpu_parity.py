@@ -218,6 +218,19 @@ def test_importance_ex_variants_parity(lengths, L, Hq, Hkv, dh, qs, tag):
     assert np.array_equal(host(estp.attn_importance_ex(Qd, Kd, cud, max(lengths))), plain)
 
 
+@pytest.mark.parametrize("f32", [False, True], ids=["bf16", "f32"])
+def test_importance_accepts_a_larger_max_seqlen(f32):
+    # max_seqlen is an upper bound on the prompt lengths (at most n_tok): a looser one changes the
+    # grids (blocks past every prompt, the list of live blocks, the head split) but not the result
+    Q, K, cu = _qk([70, 1100, 9, 300], 2, 4, 2, 64, 1.0, 21)
+    if f32:
+        Q, K = oracle.widen(Q).astype(np.float32), oracle.widen(K).astype(np.float32)
+    ref = oracle.attn_importance(Q, K, cu)
+    for max_seqlen in (1100, 1300, 1479):
+        S = host(estp.attn_importance(dev(Q), dev(K), dev(cu), max_seqlen))
+        assert np.all(np.abs(S - ref) <= S_RTOL * ref + 1e-12), max_seqlen
+
+
 def test_importance_repeatable_bitwise():
     Q, K, cu = _qk([300, 45, 600], 2, 8, 2, 128, 1.0, 6)
     Qd, Kd, cud = dev(Q), dev(K), dev(cu)
@@ -414,6 +427,25 @@ def test_combine_pool_paths(spec, d, xdtype, tag):
             check_argmax_margin(int(top[b]) - lo, e_ref[lo:hi], 1e-5 * e_ref[lo:hi].max())
         again, _, _ = estp.combine_pool(Xd, Sd, Hd, cud, max(lengths), l1, l2, a, norm)
         assert torch.equal(again, pooled)
+
+
+def test_combine_pool_accepts_a_larger_max_seqlen():
+    # a looser bound on the prompt lengths moves the call to another pooling kernel (whole prompt,
+    # length-sized slices, chunked), each within the bound of the oracle
+    g = np.random.default_rng(31)
+    lengths = [700, 650, 690, 710] * 8  # 32 prompts x 8 slices of 512 features: one per compute unit
+    n, d = sum(lengths), 4096
+    X = _bf16(g.standard_normal((n, d)).astype(np.float32))
+    S = (g.random(n) / 20).astype(np.float32)
+    Hh = (g.random(n) * 8).astype(np.float32)
+    cu = I.cu_seqlens_from_lengths(lengths)
+    e_ref, _ = oracle.combine_weights(S, Hh, cu, 0.5, 0.5, 1.0, "none")
+    p_ref = oracle.pool(X, e_ref, cu)
+    for max_seqlen in (710, 4000, 9000):
+        pooled, e, _ = estp.combine_pool(dev(X), dev(S), dev(Hh), dev(cu), max_seqlen, 0.5, 0.5, 1.0, "none")
+        np.testing.assert_allclose(host(e), e_ref, rtol=1e-4, atol=1e-12)
+        P = host(pooled)
+        assert max(rel_l2(P[b], p_ref[b]) for b in range(len(lengths))) <= POOL_RTOL, max_seqlen
 
 
 # ------------------------------------------------------------------------------------------ length head
