@@ -75,7 +75,10 @@ typedef enum estp_norm { ESTP_NORM_NONE = 0, ESTP_NORM_ZSCORE = 1, ESTP_NORM_MIN
  * without fixing its activation). */
 typedef enum estp_act { ESTP_ACT_RELU = 0, ESTP_ACT_GELU_TANH = 1 } estp_act;
 
-/* Library version, e.g. 100 for 0.1.0. */
+/* Library version, e.g. 200 for 0.2.0.  The version this header describes is
+ * ESTP_VERSION; a library whose estp_version() differs has other signatures.
+ * 0.2.0 added the vocab_argmax argument of estp_token_entropy. */
+#define ESTP_VERSION 200
 ESTP_API int estp_version(void);
 
 /* Static text for a status code. */

@@ -86,7 +86,7 @@ extern "C" {
 
 int estp_debug_checks(void) { return estp::debug_checks_enabled() ? 1 : 0; }
 
-int estp_version(void) { return 100; }
+int estp_version(void) { return ESTP_VERSION; }
 
 const char* estp_status_string(int status) {
   switch (status) {

@@ -9,6 +9,8 @@ import pytest
 import paper_2608_15592_amd as estp
 from paper_2608_15592_amd import _lib
 
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "estp.h")
 
 
@@ -28,7 +30,8 @@ def test_library_exports_every_declared_symbol():
     lib = estp.load()
     for n in _declared():
         assert hasattr(lib, n), n
-    assert lib.estp_version() >= 100
+    header = open(os.path.join(ROOT, "include", "estp.h")).read()
+    assert lib.estp_version() == int(re.search(r"#define ESTP_VERSION (\d+)", header).group(1))
     for code in range(5):
         assert lib.estp_status_string(code).startswith(b"ESTP_")
 
