@@ -164,6 +164,7 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const ui
   const uint16_t* Kg = K + size_t(l) * n_tok * krow + size_t(base) * krow + size_t(g) * DH;
 
   const int q0 = qblk * kQBlock + wave * kQPerWave;  // this wave's first query
+  auto qcb = [&](int cb) { return q0 + 32 * cb; };  // first query of column block cb
   const int q_hi = min(N, qblk * kQBlock + kQBlock);  // end of the block's queries
   const int n_kt = (q_hi - 1) / kKTile + 1;           // key tiles the block needs
 
@@ -171,7 +172,7 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const ui
   bf16x8_t bq[kNC][KS];
 #pragma unroll
   for (int cb = 0; cb < kNC; ++cb) {
-    const int qi = min(q0 + cb * 32 + col, N - 1);
+    const int qi = min(qcb(cb) + col, N - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       bq[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Qh + size_t(qi) * qrow + ks * 16 + half * 8);
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const ui
     lds_barrier();  // tile kt visible; every wave is done with buffer (kt + 1) & 1
     if (kt + 1 < n_kt) stage(kt + 1, (kt + 1) & 1);
     const int k0 = kt * kKTile;
-    if (k0 > q0 + kQPerWave - 1 || q0 >= N) continue;  // whole tile after this wave's queries
+    if (k0 > qcb(kNC - 1) + 31 || qcb(0) >= N) continue;  // whole tile after this wave's queries
     const char* kb = ktile[kt & 1];
     f32x16_t acc[2][kNC];
 #pragma unroll
@@ -218,13 +219,14 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const ui
     // running log-sum-exp (s = 1), so later tiles fold with one FMA, one exp2
     // and one add per score and no max pass; a tile that would push s past
     // 2^64 (or a lane with no reference yet) is refolded exactly with its max.
-    const bool diag = k0 + kKTile - 1 > q0;
 #pragma unroll
     for (int cb = 0; cb < kNC; ++cb) {
+      if (k0 > qcb(cb) + 31 || qcb(cb) >= N) continue;  // every key after every query: nothing to fold
+      const bool diag = k0 + kKTile - 1 > qcb(cb);
       if (diag) {
         // key k0 + rb*32 + 4*half + off(r) lies after query qi iff off(r) > qi - k0 - rb*32 - 4*half,
         // with off(r) = 8*(r/4) + r%4 a constant: one compare per score, no index arithmetic
-        const int t0 = q0 + cb * 32 + col - k0 - 4 * half;
+        const int t0 = qcb(cb) + col - k0 - 4 * half;
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
@@ -269,7 +271,7 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_lse_kernel(const ui
     const float so = __shfl_xor(s[cb], 32, 64);
     const float M = fmaxf(m[cb], mo);
     const float tot = s[cb] * fast_exp2(fmaxf(m[cb] - M, kExp2Floor)) + so * fast_exp2(fmaxf(mo - M, kExp2Floor));
-    const int qi = q0 + cb * 32 + col;
+    const int qi = qcb(cb) + col;
     if (half == 0 && qi < N) lse2[(size_t(l) * Hq + h) * n_tok + base + qi] = M + fast_log2(tot);
   }
 }
@@ -323,11 +325,12 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_colsum_kernel(const
   const float* Ll = lse2 + size_t(l) * Hq * n_tok + base;
 
   const int k0 = kblk * kKBlock + wave * kKPerWave;  // this wave's first key
+  auto kcb = [&](int cb) { return k0 + 32 * cb; };  // first key of column block cb
   // keys as B fragments, resident for the whole walk
   bf16x8_t bk[kNC][KS];
 #pragma unroll
   for (int cb = 0; cb < kNC; ++cb) {
-    const int kj = min(k0 + cb * 32 + col, N - 1);
+    const int kj = min(kcb(cb) + col, N - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       bk[cb][ks] = *reinterpret_cast<const bf16x8_t*>(Kg + size_t(kj) * krow + ks * 16 + half * 8);
@@ -366,11 +369,10 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_colsum_kernel(const
     }
     const int qb = qb_first + t / hpw;
     const int i0 = qb * kQTile;
-    if (i0 + kQTile - 1 >= k0 && k0 < N) {  // some query of the tile sees some key of this wave
+    if (i0 + kQTile - 1 >= kcb(0) && kcb(0) < N) {  // some query of the tile sees some key of this wave
       const char* qt = qtile[t & 1];
       const float4* lp = reinterpret_cast<const float4*>(ltile[t & 1]);
-      // tiles holding some query i <= (or, strict, ==) a key of this wave need the mask
-      const bool diag = i0 < k0 + kKPerWave - 1 + strict;
+      // tiles holding some query i <= (or, strict, ==) a key of a column block need the mask
       // The tile's 32-query row blocks go one after another through the same
       // accumulators: the tile, and so the barrier, is twice as long as one
       // 32 x 64 block of scores without a second set of registers.
@@ -400,11 +402,14 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_colsum_kernel(const
         }
 #pragma unroll
         for (int cb = 0; cb < kNC; ++cb) {
+          // every query of the row block before every key of the column block (or past the prompt)
+          if (i0 + rb * 32 + 31 < kcb(cb) + strict || kcb(cb) >= N) continue;
+          const bool diag = i0 < kcb(cb) + 31 + strict;
           float cs = 0.f;
           if (diag) {
             // query i = i0 + rb*32 + 4*half + off(r) counts for key j iff j < i + 1 - strict, i.e.
             // off(r) > j - i0 - rb*32 - 4*half - 1 + strict with off(r) = 8*(r/4) + r%4 a constant
-            const int t = k0 + cb * 32 + col - i0 - rb * 32 - 4 * half - 1 + strict;
+            const int t = kcb(cb) + col - i0 - rb * 32 - 4 * half - 1 + strict;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
               const float p = fast_exp2(fmaf(acc[cb][r], c2, -lr[r]));
@@ -424,7 +429,7 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void attn_colsum_kernel(const
 #pragma unroll
   for (int cb = 0; cb < kNC; ++cb) {
     csum[cb] += __shfl_xor(csum[cb], 32, 64);
-    const int j = k0 + cb * 32 + col;
+    const int j = kcb(cb) + col;
     if (half == 0 && j < N) part[((size_t(l) * Hkv + g) * nsplit + hs) * n_tok + base + j] = csum[cb];
   }
 }
